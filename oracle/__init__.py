@@ -1,0 +1,199 @@
+"""Oracle for the co-activation routing path (test infrastructure only).
+
+A ctypes wrapper over liboracle.so, the plain single-threaded C statement of
+the path in cobalt_oracle.c. Only tests/, the smoke check and the benchmark's
+CPU-baseline leg may import this package; the library under
+paper_2609_36959_amd/ never does, and shares no code with it.
+
+All functions take and return numpy arrays on the host.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboracle.so")
+SRC_PATH = os.path.join(_HERE, "cobalt_oracle.c")
+
+# -ffp-contract=off keeps every multiply and add separately rounded except
+# the explicit fmaf of the combine.
+CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
+
+
+def build(verbose: bool = False) -> str:
+    cmd = ["gcc", *CFLAGS, SRC_PATH, "-o", LIB_PATH + ".tmp", "-lm"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(LIB_PATH + ".tmp", LIB_PATH)
+    return LIB_PATH
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH) or os.path.getmtime(LIB_PATH) < os.path.getmtime(SRC_PATH):
+            build()
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        i32, i64, u32, u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64
+        L.ref_splitmix64.argtypes = [u64]
+        L.ref_splitmix64.restype = u64
+        L.ref_rng_key.argtypes = [u64, u64]
+        L.ref_rng_key.restype = u64
+        L.ref_pick.argtypes = [u64, u64, u32, u32]
+        L.ref_pick.restype = u32
+        L.ref_bf16_to_f32.argtypes = [ctypes.c_uint16]
+        L.ref_bf16_to_f32.restype = ctypes.c_float
+        L.ref_f32_to_bf16.argtypes = [ctypes.c_float]
+        L.ref_f32_to_bf16.restype = ctypes.c_uint16
+        L.ref_coact_stats.argtypes = [P, i64, i32, i32, P, P]
+        L.ref_layout_tables.argtypes = [i32, i32, i32, i32, P, P, P, P, P]
+        L.ref_assign.argtypes = [i32, i32, i32, P, P, P, P, P, i64, i32, u64, u64, i32, P, P]
+        L.ref_dispatch.argtypes = [P, P, i64, i32, i32, P, i64, P, P, P, P]
+        L.ref_combine.argtypes = [P, i64, P, P, i64, i32, i64, P, P]
+        L.ref_traffic.argtypes = [P, P, i64, i32, i32, i32, P, P, P]
+        for f in ("ref_coact_stats", "ref_layout_tables", "ref_assign", "ref_dispatch",
+                  "ref_combine", "ref_traffic"):
+            getattr(L, f).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise OracleError(f"{what} failed with status {rc}")
+
+
+# ---------------------------------------------------------------- scalars
+def splitmix64(z: int) -> int:
+    return int(lib().ref_splitmix64(z & (2**64 - 1)))
+
+
+def rng_key(seed: int, step: int) -> int:
+    return int(lib().ref_rng_key(seed & (2**64 - 1), step & (2**64 - 1)))
+
+
+def pick(key: int, p: int, stream: int, cnt: int) -> int:
+    return int(lib().ref_pick(key, p, stream, cnt))
+
+
+def bf16_to_f32(bits) -> np.ndarray:
+    bits = np.asarray(bits, dtype=np.uint16).ravel()
+    f = lib().ref_bf16_to_f32
+    return np.array([f(int(b)) for b in bits], dtype=np.float32)
+
+
+def f32_to_bf16(vals) -> np.ndarray:
+    vals = np.asarray(vals, dtype=np.float32).ravel()
+    f = lib().ref_f32_to_bf16
+    return np.array([f(float(v)) for v in vals], dtype=np.uint16)
+
+
+# ---------------------------------------------------------------- path steps
+def coact_stats(topk, E, coact=None, count=None):
+    """Adds into coact [E, E] uint32 and count [E] uint32 (fresh if None)."""
+    topk = _c(topk, np.int32)
+    T, K = topk.shape
+    coact = np.zeros((E, E), np.uint32) if coact is None else coact
+    count = np.zeros(E, np.uint32) if count is None else count
+    assert coact.dtype == np.uint32 and coact.flags.c_contiguous
+    assert count.dtype == np.uint32 and count.flags.c_contiguous
+    _check(lib().ref_coact_stats(_p(topk), T, K, E, _p(coact), _p(count)), "coact_stats")
+    return coact, count
+
+
+def layout_tables(N, g, E, slot_table, owner=None):
+    """Returns (node_mask [E] u32, rank_mask [E, N] u32, owner [E] i32)."""
+    st = _c(slot_table, np.int32)
+    G, S = st.shape
+    assert G == N * g
+    own_in = _c(owner, np.int32)
+    node_mask = np.zeros(E, np.uint32)
+    rank_mask = np.zeros((E, N), np.uint32)
+    own = np.zeros(E, np.int32)
+    _check(lib().ref_layout_tables(N, g, E, S, _p(st), _p(own_in), _p(node_mask),
+                                   _p(rank_mask), _p(own)), "layout_tables")
+    return node_mask, rank_mask, own
+
+
+def assign(N, g, E, tables, topk, src=None, seed=0, step=0, mode=0):
+    """Algorithm 1 (mode 0) or owner-only (mode 1).
+    Returns (assigned [T, K] i32, remote_nodes [T] u16)."""
+    node_mask, rank_mask, owner = tables
+    topk = _c(topk, np.int32)
+    T, K = topk.shape
+    src = _c(src, np.int32)
+    out = np.zeros((T, K), np.int32)
+    rn = np.zeros(T, np.uint16)
+    _check(lib().ref_assign(N, g, E, _p(_c(node_mask, np.uint32)), _p(_c(rank_mask, np.uint32)),
+                            _p(_c(owner, np.int32)), _p(topk), _p(src), T, K,
+                            seed & (2**64 - 1), step & (2**64 - 1), mode, _p(out), _p(rn)),
+           "assign")
+    return out, rn
+
+
+def dispatch(assigned, G, src=None, x=None, d=0):
+    """Returns (counts [G, G] i32, offsets [G*G+1] i64, pos [T, K] i32,
+    packed [T*K, d] u16 or None). x is bf16 bits as uint16 [T, d]."""
+    assigned = _c(assigned, np.int32)
+    T, K = assigned.shape
+    src = _c(src, np.int32)
+    counts = np.zeros((G, G), np.int32)
+    offsets = np.zeros(G * G + 1, np.int64)
+    pos = np.zeros((T, K), np.int32)
+    packed = None
+    if x is not None:
+        x = _c(x, np.uint16)
+        d = x.shape[1]
+        packed = np.zeros((T * K, d), np.uint16)
+    _check(lib().ref_dispatch(_p(assigned), _p(src), T, K, G, _p(x), d, _p(counts),
+                              _p(offsets), _p(pos), _p(packed)), "dispatch")
+    return counts, offsets, pos, packed
+
+
+def combine(expert_out, pos, gates):
+    """expert_out: uint16 bf16 bits [rows, d]; pos [T, K]; gates [T, K] f32.
+    Returns (y bf16 bits [T, d] u16, y32 [T, d] f32)."""
+    eo = _c(expert_out, np.uint16)
+    rows, d = eo.shape
+    pos = _c(pos, np.int32)
+    gates = _c(gates, np.float32)
+    T, K = pos.shape
+    y = np.zeros((T, d), np.uint16)
+    y32 = np.zeros((T, d), np.float32)
+    _check(lib().ref_combine(_p(eo), rows, _p(pos), _p(gates), T, K, d, _p(y), _p(y32)),
+           "combine")
+    return y, y32
+
+
+def traffic(assigned, N, g, src=None):
+    """Returns (V, cross_pairs, load [G] i64) of Eq. 1."""
+    assigned = _c(assigned, np.int32)
+    T, K = assigned.shape
+    src = _c(src, np.int32)
+    V = ctypes.c_int64()
+    cp = ctypes.c_int64()
+    load = np.zeros(N * g, np.int64)
+    _check(lib().ref_traffic(_p(assigned), _p(src), T, K, N, g, ctypes.byref(V),
+                             ctypes.byref(cp), _p(load)), "traffic")
+    return V.value, cp.value, load

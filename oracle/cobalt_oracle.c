@@ -1,0 +1,399 @@
+/*
+ * Oracle for the co-activation token-routing path of Cobalt
+ * ("Leveraging Expert Co-activation for Efficient Distributed MoE Training").
+ *
+ * TEST INFRASTRUCTURE ONLY. This is a plain, slow, single-threaded C
+ * statement of what the routing path computes, used to check the HIP
+ * library. Only the test suite, the smoke check and the benchmark's CPU
+ * baseline leg may load it. It shares no source, header, table or helper
+ * with the HIP library; the two agree only through the definitions below.
+ *
+ * Every loop runs in index order; nothing is blocked, fused or reordered.
+ *
+ * Pins (what checks this file against something other than itself) are in
+ * tests/test_oracle_*.py. One part is "parity unpinned" by the paper: WHICH
+ * replica RandomNode / UniformChoice return (Algorithm 1 only says the
+ * choice is random, and uniform for ranks). The counter-based draw below is
+ * this implementation's reading, pinned by SplitMix64's published outputs
+ * and by uniformity tests, not by any value in the paper.
+ *
+ * Notation (Section 3.1): T tokens, E experts, K selections per token,
+ * N nodes of g ranks, G = N*g ranks, node(r) = r / g. Pair p = t*K + j is
+ * slot j of token t.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define REF_OK 0
+#define REF_EINVAL 1
+#define REF_EDATA 5
+
+/* ---------------------------------------------------------------------- */
+/* SplitMix64 (Steele, Lea & Flood, "Fast splittable pseudorandom number   */
+/* generators", OOPSLA 2014): the generator advances its state by the      */
+/* golden-ratio increment 0x9e3779b97f4a7c15 and returns a mix of the new  */
+/* state. ref_splitmix64(z) is the output produced from state z.           */
+/* ---------------------------------------------------------------------- */
+uint64_t ref_splitmix64(uint64_t z)
+{
+    z += 0x9e3779b97f4a7c15ULL;
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+    return z ^ (z >> 31);
+}
+
+/* Key of one (seed, step): every draw of that step hashes the pair index
+ * with it. */
+uint64_t ref_rng_key(uint64_t seed, uint64_t step)
+{
+    return ref_splitmix64(ref_splitmix64(seed) ^ step);
+}
+
+/* Uniform index in [0, cnt) for pair p and draw stream s (0 = node,
+ * 1 = rank): the high 32 bits of the hash scaled by cnt (multiply-shift
+ * range reduction, Lemire 2019). */
+uint32_t ref_pick(uint64_t key, uint64_t p, uint32_t stream, uint32_t cnt)
+{
+    uint64_t h = ref_splitmix64(key ^ ((p << 1) | (uint64_t)stream));
+    return (uint32_t)(((h >> 32) * (uint64_t)cnt) >> 32);
+}
+
+/* ---------------------------------------------------------------------- */
+/* bf16 <-> fp32 from the IEEE-754 bit layout: bf16 is the top 16 bits of  */
+/* an fp32. Narrowing rounds to nearest, ties to even; NaN stays a quiet   */
+/* NaN with its sign.                                                      */
+/* ---------------------------------------------------------------------- */
+float ref_bf16_to_f32(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+
+uint16_t ref_f32_to_bf16(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu) != 0)
+        return (uint16_t)((u >> 16) | 0x0040u);
+    uint32_t upper = u >> 16;
+    uint32_t lower = u & 0xffffu;
+    if (lower > 0x8000u || (lower == 0x8000u && (upper & 1u)))
+        upper += 1; /* may carry into the exponent: correct rounding to inf */
+    return (uint16_t)upper;
+}
+
+static int popcount32(uint32_t v)
+{
+    int c = 0;
+    while (v) { c += (int)(v & 1u); v >>= 1; }
+    return c;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Co-activation statistics (Section 3.2, Stage 1): c_ij counts the tokens */
+/* that select both experts i and j, w_e the tasks of expert e. Raw counts */
+/* are added into coact [E][E] for every ordered pair of distinct slots,   */
+/* and into count [E] for every selection; both accumulate across calls.   */
+/* ---------------------------------------------------------------------- */
+int ref_coact_stats(const int32_t* topk, int64_t T, int32_t K, int32_t E,
+                    uint32_t* coact, uint32_t* count)
+{
+    if (T < 0 || K < 1 || E < 1) return REF_EINVAL;
+    for (int64_t t = 0; t < T; ++t)
+        for (int32_t a = 0; a < K; ++a) {
+            int32_t ea = topk[t * K + a];
+            if (ea < 0 || ea >= E) return REF_EDATA;
+        }
+    for (int64_t t = 0; t < T; ++t) {
+        const int32_t* D = topk + t * K;
+        for (int32_t a = 0; a < K; ++a) {
+            if (count) count[D[a]] += 1u;
+            for (int32_t b = 0; b < K; ++b)
+                if (a != b) coact[(int64_t)D[a] * E + D[b]] += 1u;
+        }
+    }
+    return REF_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Layout tables from the replica table (Section 3.1, layout {P_r};        */
+/* Section 3.3, R_{e,n} and N_e).                                          */
+/*   node_mask[e]     bit n set iff some rank of node n holds e  (N_e)     */
+/*   rank_mask[e*N+n] bit i set iff rank n*g+i holds e           (R_{e,n}) */
+/*   owner_out[e]     owner_in[e] if given, else the lowest rank holding e */
+/* Rejected (REF_EDATA): an expert with no replica (coverage, Eq. 2), an   */
+/* expert twice on one rank (Stage 2 placement rule), an owner that does   */
+/* not hold its expert, an id outside [-1, E).                             */
+/* ---------------------------------------------------------------------- */
+int ref_layout_tables(int32_t N, int32_t g, int32_t E, int32_t S,
+                      const int32_t* slot_table, const int32_t* owner_in,
+                      uint32_t* node_mask, uint32_t* rank_mask, int32_t* owner_out)
+{
+    if (N < 1 || N > 16 || g < 1 || g > 32 || E < 1 || S < 1) return REF_EINVAL;
+    int32_t G = N * g;
+    for (int32_t e = 0; e < E; ++e) {
+        node_mask[e] = 0;
+        owner_out[e] = -1;
+        for (int32_t n = 0; n < N; ++n) rank_mask[e * N + n] = 0;
+    }
+    for (int32_t r = 0; r < G; ++r) {
+        int32_t n = r / g, i = r % g;
+        for (int32_t s = 0; s < S; ++s) {
+            int32_t e = slot_table[r * S + s];
+            if (e == -1) continue;
+            if (e < 0 || e >= E) return REF_EDATA;
+            if (rank_mask[e * N + n] & (1u << i)) return REF_EDATA;
+            rank_mask[e * N + n] |= 1u << i;
+            node_mask[e] |= 1u << n;
+            if (owner_out[e] < 0) owner_out[e] = r;
+        }
+    }
+    for (int32_t e = 0; e < E; ++e) {
+        if (node_mask[e] == 0) return REF_EDATA;
+        if (owner_in) {
+            int32_t o = owner_in[e];
+            if (o < 0 || o >= G) return REF_EDATA;
+            if (!(rank_mask[e * N + o / g] & (1u << (o % g)))) return REF_EDATA;
+            owner_out[e] = o;
+        }
+    }
+    return REF_OK;
+}
+
+/* RemoteMask (Section 3.3, step 1): the (N-1)-bit mask of the remote nodes
+ * of a node set, where bit i stands for the i-th node other than `home`
+ * in ascending id. */
+static uint32_t remote_mask(uint32_t nodes, int32_t home, int32_t N)
+{
+    uint32_t m = 0;
+    int32_t bit = 0;
+    for (int32_t n = 0; n < N; ++n) {
+        if (n == home) continue;
+        if (nodes & (1u << n)) m |= 1u << bit;
+        ++bit;
+    }
+    return m;
+}
+
+/* Node id of remote bit i (inverse of remote_mask's numbering). */
+static int32_t remote_node(int32_t i, int32_t home)
+{
+    return i < home ? i : i + 1;
+}
+
+/* i-th (0-based) set bit of v, counting up from bit 0. */
+static int32_t nth_set_bit(uint32_t v, uint32_t i)
+{
+    for (int32_t b = 0; b < 32; ++b)
+        if (v & (1u << b)) {
+            if (i == 0) return b;
+            --i;
+        }
+    return -1;
+}
+
+static int32_t src_of(const int32_t* src, int64_t t, int64_t T, int32_t G)
+{
+    return src ? src[t] : (int32_t)(t / (T / G));
+}
+
+/* ---------------------------------------------------------------------- */
+/* Communication-aware task assignment (Section 3.3, Algorithm 1).         */
+/* mode 0: Algorithm 1. mode 1: every task on its expert's owner rank (the */
+/* owner-only baseline that the paper compares against).                  */
+/* assigned [T][K]: r_te. remote_nodes [T] (nullable): bit n set iff node  */
+/* n != node(s_t) receives token t.                                        */
+/* There is no load cap (Section 3.3: balance comes from the layout and    */
+/* the uniform draw).                                                      */
+/* ---------------------------------------------------------------------- */
+int ref_assign(int32_t N, int32_t g, int32_t E,
+               const uint32_t* node_mask, const uint32_t* rank_mask, const int32_t* owner,
+               const int32_t* topk, const int32_t* src, int64_t T, int32_t K,
+               uint64_t seed, uint64_t step, int32_t mode,
+               int32_t* assigned, uint16_t* remote_nodes)
+{
+    int32_t G = N * g;
+    if (N < 1 || N > 16 || g < 1 || g > 32 || K < 1 || K > 64 || T < 0) return REF_EINVAL;
+    if (!src && T % G != 0) return REF_EINVAL;
+    uint64_t key = ref_rng_key(seed, step);
+    int32_t U[64];
+    uint32_t m[64];
+    int32_t node_of[64];
+
+    for (int64_t t = 0; t < T; ++t) {
+        const int32_t* D = topk + t * K;
+        int32_t s_t = src_of(src, t, T, G);
+        if (s_t < 0 || s_t >= G) return REF_EDATA;
+        for (int32_t j = 0; j < K; ++j)
+            if (D[j] < 0 || D[j] >= E) return REF_EDATA;
+        int32_t home = s_t / g;
+
+        if (mode == 1) {
+            uint32_t nodes = 0;
+            for (int32_t j = 0; j < K; ++j) {
+                int32_t r = owner[D[j]];
+                assigned[t * K + j] = r;
+                if (r / g != home) nodes |= 1u << (r / g);
+            }
+            if (remote_nodes) remote_nodes[t] = (uint16_t)nodes;
+            continue;
+        }
+
+        /* Step 1: select execution nodes. U_t holds the selected experts
+         * with no replica on the source node; each gets its remote mask. */
+        int32_t nU = 0;
+        for (int32_t j = 0; j < K; ++j) {
+            uint32_t Ne = node_mask[D[j]];
+            if (!(Ne & (1u << home))) {
+                U[nU] = j;
+                m[nU] = remote_mask(Ne, home, N);
+                ++nU;
+            }
+        }
+        /* Start from all remote nodes, then scan every smaller candidate in
+         * increasing value and keep a feasible one with strictly fewer
+         * nodes: the first feasible minimum cover wins. */
+        uint32_t full = (N > 1) ? ((1u << (N - 1)) - 1u) : 0u;
+        uint32_t bstar = full;
+        for (uint32_t b = 0; N > 1 && b + 1u <= full; ++b) {
+            int feasible = 1;
+            for (int32_t u = 0; u < nU; ++u)
+                if ((b & m[u]) == 0) { feasible = 0; break; }
+            if (feasible && popcount32(b) < popcount32(bstar)) bstar = b;
+        }
+        /* Each expert of U_t goes to a random node among the chosen ones
+         * that hold it; the other experts stay on the source node. */
+        for (int32_t j = 0; j < K; ++j) node_of[j] = home;
+        for (int32_t u = 0; u < nU; ++u) {
+            uint32_t cand = bstar & m[u];
+            int64_t p = t * K + U[u];
+            uint32_t k = ref_pick(key, (uint64_t)p, 0, (uint32_t)popcount32(cand));
+            node_of[U[u]] = remote_node(nth_set_bit(cand, k), home);
+        }
+        /* Step 2: select execution ranks uniformly among the node's ranks
+         * that hold the expert. */
+        for (int32_t j = 0; j < K; ++j) {
+            int32_t n = node_of[j];
+            uint32_t R = rank_mask[D[j] * N + n];
+            int64_t p = t * K + j;
+            uint32_t k = ref_pick(key, (uint64_t)p, 1, (uint32_t)popcount32(R));
+            assigned[p] = n * g + nth_set_bit(R, k);
+        }
+        if (remote_nodes) {
+            uint32_t nodes = 0;
+            for (int32_t i = 0; i < N - 1; ++i)
+                if (bstar & (1u << i)) nodes |= 1u << remote_node(i, home);
+            remote_nodes[t] = (uint16_t)nodes;
+        }
+    }
+    return REF_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Dispatch layout (the EP dispatch of Section 1 / Fig. 1, one row per    */
+/* (token, expert) pair). Bucket of pair p = (s_t, r_p), buckets in        */
+/* row-major order; each bucket keeps pairs in increasing p.               */
+/*   counts [G][G]      pairs per (source, destination)                    */
+/*   offsets [G*G+1]    exclusive prefix sum of counts, offsets[G*G]=total */
+/*   pos [T][K]         row of pair p in the packed buffer                 */
+/*   packed [T*K][d]    packed[pos[p]] = x[t] (bf16 bits), nullable        */
+/* ---------------------------------------------------------------------- */
+int ref_dispatch(const int32_t* assigned, const int32_t* src, int64_t T, int32_t K, int32_t G,
+                 const uint16_t* x, int64_t d,
+                 int32_t* counts, int64_t* offsets, int32_t* pos, uint16_t* packed)
+{
+    if (T < 0 || K < 1 || G < 1 || d < 0) return REF_EINVAL;
+    if (!src && T % G != 0) return REF_EINVAL;
+    int64_t GG = (int64_t)G * G;
+    for (int64_t b = 0; b < GG; ++b) counts[b] = 0;
+    for (int64_t t = 0; t < T; ++t) {
+        int32_t s = src_of(src, t, T, G);
+        if (s < 0 || s >= G) return REF_EDATA;
+        for (int32_t j = 0; j < K; ++j) {
+            int32_t r = assigned[t * K + j];
+            if (r < 0 || r >= G) return REF_EDATA;
+            counts[(int64_t)s * G + r] += 1;
+        }
+    }
+    int64_t run = 0;
+    for (int64_t b = 0; b < GG; ++b) {
+        offsets[b] = run;
+        run += counts[b];
+    }
+    offsets[GG] = run;
+    int64_t* cursor = (int64_t*)malloc((size_t)(GG > 0 ? GG : 1) * sizeof(int64_t));
+    if (!cursor) return REF_EINVAL;
+    for (int64_t b = 0; b < GG; ++b) cursor[b] = offsets[b];
+    for (int64_t t = 0; t < T; ++t) {
+        int32_t s = src_of(src, t, T, G);
+        for (int32_t j = 0; j < K; ++j) {
+            int64_t p = t * K + j;
+            int64_t b = (int64_t)s * G + assigned[p];
+            int64_t row = cursor[b]++;
+            pos[p] = (int32_t)row;
+            if (packed)
+                for (int64_t c = 0; c < d; ++c) packed[row * d + c] = x[t * d + c];
+        }
+    }
+    free(cursor);
+    return REF_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Combine and weighted sum (Fig. 1, last stage): token t gets            */
+/*   y[t][c] = bf16( sum_j gates[t][j] * expert_out[pos[t][j]][c] )       */
+/* accumulated in fp32 from 0, one fused multiply-add per slot, j = 0..K-1.*/
+/* y32 (nullable) receives the fp32 sums. Rows outside [0, rows) add 0.    */
+/* ---------------------------------------------------------------------- */
+int ref_combine(const uint16_t* expert_out, int64_t rows, const int32_t* pos, const float* gates,
+                int64_t T, int32_t K, int64_t d, uint16_t* y, float* y32)
+{
+    if (T < 0 || K < 1 || d < 0) return REF_EINVAL;
+    for (int64_t t = 0; t < T; ++t)
+        for (int64_t c = 0; c < d; ++c) {
+            float acc = 0.0f;
+            for (int32_t j = 0; j < K; ++j) {
+                int64_t row = pos[t * K + j];
+                if (row < 0 || row >= rows) continue;
+                acc = fmaf(gates[t * K + j], ref_bf16_to_f32(expert_out[row * d + c]), acc);
+            }
+            if (y) y[t * d + c] = ref_f32_to_bf16(acc);
+            if (y32) y32[t * d + c] = acc;
+        }
+    return REF_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Traffic model (Eq. 1) and load: V = sum over tokens of the number of    */
+/* distinct nodes other than node(s_t) among the token's assigned ranks;   */
+/* cross_pairs counts pairs whose rank is on another node; load[r] counts  */
+/* pairs assigned to rank r (w summed over the rank's replicas).           */
+/* ---------------------------------------------------------------------- */
+int ref_traffic(const int32_t* assigned, const int32_t* src, int64_t T, int32_t K,
+                int32_t N, int32_t g, int64_t* V, int64_t* cross_pairs, int64_t* load)
+{
+    int32_t G = N * g;
+    if (!src && T % G != 0) return REF_EINVAL;
+    *V = 0;
+    *cross_pairs = 0;
+    for (int32_t r = 0; r < G; ++r) load[r] = 0;
+    for (int64_t t = 0; t < T; ++t) {
+        int32_t home = src_of(src, t, T, G) / g;
+        uint32_t nodes = 0;
+        for (int32_t j = 0; j < K; ++j) {
+            int32_t r = assigned[t * K + j];
+            if (r < 0 || r >= G) return REF_EDATA;
+            load[r] += 1;
+            if (r / g != home) {
+                nodes |= 1u << (r / g);
+                *cross_pairs += 1;
+            }
+        }
+        *V += popcount32(nodes);
+    }
+    return REF_OK;
+}
