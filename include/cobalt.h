@@ -1,0 +1,184 @@
+/*
+ * cobalt.h - C ABI of the co-activation token-routing path of Cobalt
+ * ("Leveraging Expert Co-activation for Efficient Distributed MoE Training").
+ *
+ * One MoE layer, one training step, on one GPU. G = N * gpus_per_node
+ * virtual ranks on N virtual nodes; node(r) = r / gpus_per_node. T tokens,
+ * each with K selected experts out of E (topk_idx[t][j], slot j). Pair
+ * p = t*K + j is the task (t, topk_idx[t][j]).
+ *
+ * Conventions for every call below:
+ *  - Pointers are DEVICE pointers unless the name starts with host_.
+ *  - Arrays are dense, row-major, in the element type of the declaration;
+ *    bf16 rows are raw 16-bit patterns, 16-byte aligned.
+ *  - The caller owns every buffer. The four path calls (cobalt_coact_stats,
+ *    cobalt_assign, cobalt_dispatch_pack, cobalt_combine) allocate nothing,
+ *    enqueue their kernels on `stream` (a hipStream_t; NULL = the default
+ *    stream of the current device) and return without synchronising.
+ *  - Errors are reported by return code only. Argument checks run on the
+ *    host before anything is enqueued; on any error nothing is enqueued and
+ *    no output is touched. Data-dependent checks (expert ids in range,
+ *    distinct experts per token, non-decreasing source ranks) are made only
+ *    by cobalt_validate_routing: on data that fails them the path calls do
+ *    not read or write outside the buffers they were given, but their
+ *    results are unspecified.
+ *  - Calls on distinct (layout, stream, output buffers) may run concurrently.
+ */
+#ifndef COBALT_H
+#define COBALT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    COBALT_OK = 0,
+    COBALT_EINVAL = 1,       /* bad argument (null pointer, size out of range, misaligned) */
+    COBALT_EUNSUPPORTED = 2, /* valid request outside this build's limits */
+    COBALT_ENOMEM = 3,       /* device allocation failed (layout calls only) */
+    COBALT_EHIP = 4,         /* a HIP runtime call or kernel launch failed */
+    COBALT_EDATA = 5         /* input data violates the model (layout or routing) */
+} cobalt_status;
+
+/* Limits of this build: 1 <= N <= 16, 1 <= gpus_per_node <= 32,
+ * G = N * gpus_per_node <= 512, 1 <= K <= 16, 1 <= E <= 4096,
+ * T * K < 2^31, d % 8 == 0 (rows are whole 16-byte vectors). */
+
+const char* cobalt_status_string(cobalt_status s);
+
+/* ------------------------------------------------------------------------
+ * Expert layout {P_r} (Section 3.1, "Problem formulation"; the per-expert
+ * sets R_{e,n} and N_e of Section 3.3, step 1).
+ *
+ * host_slot_table [G][S]: expert ids held by rank r, -1 = empty slot.
+ * host_owner_rank [E]:    owner rank of each expert (used by the owner-only
+ *                         baseline of cobalt_assign), or NULL = the lowest
+ *                         rank holding the expert.
+ * The layout is rejected with COBALT_EDATA if an expert has no replica
+ * (coverage constraint of Eq. 2), a rank holds an expert twice (placement
+ * rule of Section 3.2, Stage 2), an owner does not hold its expert, or an
+ * id lies outside [-1, E). The slot budget S = (1+rho)E/G of Eq. 2 is the
+ * table's width.
+ * Derives node_mask[e] (bit n: e on node n), rank_mask[e][n] (bit i: e on
+ * rank n*g+i) and the candidate-cover order used by cobalt_assign, and
+ * copies them to the current device. Synchronous; the handle belongs to
+ * the device current at creation and may only be used there.
+ * ---------------------------------------------------------------------- */
+typedef struct cobalt_layout_s* cobalt_layout_t;
+
+cobalt_status cobalt_layout_create(int32_t N, int32_t gpus_per_node, int32_t E, int32_t S,
+                                   const int32_t* host_slot_table,
+                                   const int32_t* host_owner_rank,
+                                   cobalt_layout_t* out);
+cobalt_status cobalt_layout_destroy(cobalt_layout_t layout);
+
+/* Copies the derived tables back to the host (synchronous): node_mask [E],
+ * rank_mask [E][N], owner_rank [E]. Any output may be NULL. */
+cobalt_status cobalt_layout_tables(cobalt_layout_t layout, uint32_t* host_node_mask,
+                                   uint32_t* host_rank_mask, int32_t* host_owner_rank);
+
+/* ------------------------------------------------------------------------
+ * Step 1: co-activation statistics (Section 3.2, Stage 1: c_ij counts the
+ * tokens that select both experts i and j; w_e counts the tasks of e).
+ *
+ * topk_idx [T][K] int32 in, coact [E][E] uint32 in/out, expert_count [E]
+ * uint32 in/out (may be NULL).
+ * For every token and every ordered pair of distinct slots (a, b):
+ * coact[topk_idx[t][a]][topk_idx[t][b]] += 1; for every slot:
+ * expert_count[topk_idx[t][a]] += 1. Nothing is zeroed: counts accumulate
+ * across calls (and steps) until the caller clears them. With distinct
+ * experts per token coact is symmetric with a zero diagonal and row sums
+ * (K-1) * expert_count.
+ * ---------------------------------------------------------------------- */
+cobalt_status cobalt_coact_stats(const int32_t* topk_idx, int64_t T, int32_t K, int32_t E,
+                                 uint32_t* coact, uint32_t* expert_count, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Step 2: communication-aware task assignment (Section 3.3, Algorithm 1).
+ *
+ * topk_idx [T][K] int32 in; src_rank [T] int32 in, the source rank s_t of
+ * each token, non-decreasing, or NULL = contiguous blocks s_t = t / (T/G)
+ * (then T % G must be 0).
+ * mode 0 = Algorithm 1: the experts held on the source node run there; the
+ *   rest are covered by the fewest remote nodes (the first cover in order of
+ *   (node count, remote-node bitmask), where remote bit i is the i-th node
+ *   other than node(s_t)); each such expert draws one of the chosen nodes
+ *   holding it, then every task draws one rank of its node holding the
+ *   expert. No load cap is applied.
+ * mode 1 = owner-only baseline: every task runs on its expert's owner rank.
+ * Draws are counter-based: with sm(z) the SplitMix64 output for state z
+ * (Steele, Lea & Flood 2014), key = sm(sm(seed) ^ step),
+ * h = sm(key ^ (p << 1 | s)) for pair p and draw s (0 = node, 1 = rank),
+ * and the drawn index among c candidates (set bits, ascending) is
+ * ((h >> 32) * c) >> 32.
+ * assigned_rank [T][K] int32 out: r_te per pair. remote_nodes [T] uint16
+ * out (may be NULL): bit n set iff node n != node(s_t) receives token t
+ * (its popcount is the token's term of Eq. 1).
+ * ---------------------------------------------------------------------- */
+cobalt_status cobalt_assign(cobalt_layout_t layout, const int32_t* topk_idx,
+                            const int32_t* src_rank, int64_t T, int32_t K,
+                            uint64_t seed, uint64_t step, int32_t mode,
+                            int32_t* assigned_rank, uint16_t* remote_nodes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Step 3: dispatch layout and pack (the EP dispatch all-to-all's send side,
+ * Section 1 and Fig. 1; here one row per (token, expert) pair).
+ *
+ * Bucket of pair p: (s_t, r_p). Buckets are laid out in row-major order
+ * (per-source send buffers, each split by destination rank), and each
+ * bucket keeps its pairs in increasing p.
+ * assigned_rank [T][K] int32 in; src_rank as in cobalt_assign;
+ * x [T][d] bf16 in (may be NULL together with packed: layout only).
+ * send_counts [G][G] int32 out: pairs per (source, destination).
+ * send_offsets [G*G+1] int64 out: exclusive prefix sum of send_counts,
+ *   send_offsets[G*G] = number of pairs placed (T*K on valid data).
+ * pos [T][K] int32 out: packed row of each pair.
+ * packed [T*K][d] bf16 out: packed[pos[p]] = x[t], bit for bit.
+ * workspace: device scratch of at least cobalt_dispatch_workspace_bytes(T,
+ *   K, G) bytes, 256-byte aligned, owned by the caller; contents on entry
+ *   are ignored; it must not be shared by calls that may overlap.
+ * ---------------------------------------------------------------------- */
+size_t cobalt_dispatch_workspace_bytes(int64_t T, int32_t K, int32_t G);
+
+cobalt_status cobalt_dispatch_pack(const int32_t* assigned_rank, const int32_t* src_rank,
+                                   int64_t T, int32_t K, int32_t G,
+                                   const void* x, int64_t d,
+                                   int32_t* send_counts, int64_t* send_offsets,
+                                   int32_t* pos, void* packed,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Step 4: combine and weighted sum (Fig. 1, last stage).
+ *
+ * expert_out [T*K][d] bf16 in, in the packed layout (row pos[p] holds the
+ * result of pair p); pos [T][K] int32 in; gates [T][K] fp32 in.
+ * y [T][d] bf16 out:
+ *   y[t][c] = bf16_rne( sum_{j=0..K-1} gates[t][j] * expert_out[pos[t][j]][c] )
+ * accumulated in fp32 from 0 with one fused multiply-add per slot in slot
+ * order. y_f32 [T][d] fp32 out (may be NULL) receives the fp32 sums. A pos
+ * outside [0, T*K) contributes nothing.
+ * ---------------------------------------------------------------------- */
+cobalt_status cobalt_combine(const void* expert_out, const int32_t* pos, const float* gates,
+                             int64_t T, int32_t K, int64_t d,
+                             void* y, float* y_f32, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Debug check of routing inputs (synchronous; allocates a few bytes).
+ * Checks 0 <= topk_idx < E, distinct experts within each token, and, if
+ * src_rank is given, 0 <= src_rank < G and non-decreasing. Returns COBALT_OK
+ * or COBALT_EDATA; host_flags (may be NULL) receives a bitmask:
+ * 1 = expert id out of range, 2 = duplicate expert in a token,
+ * 4 = source rank out of range, 8 = source ranks decreasing.
+ * ---------------------------------------------------------------------- */
+cobalt_status cobalt_validate_routing(const int32_t* topk_idx, const int32_t* src_rank,
+                                      int64_t T, int32_t K, int32_t E, int32_t G,
+                                      uint32_t* host_flags, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COBALT_H */

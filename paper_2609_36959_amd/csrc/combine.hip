@@ -1,0 +1,130 @@
+// Combine and weighted sum (Fig. 1, last stage): one wave per token. Each
+// lane owns 16-byte column chunks of the output row; for a chunk it loads
+// the K expert-output chunks (pos[t][j]-th packed rows) first, then folds
+// them into eight fp32 accumulators with one fused multiply-add per slot in
+// slot order, and stores the round-to-nearest-even bf16 result (plus the
+// fp32 sums when asked).
+#include "internal.hpp"
+
+namespace cobalt {
+namespace {
+
+constexpr int kCombineWaves = 4;
+
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (u >> 16) | 0x40u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <bool kF32>
+__global__ __launch_bounds__(kCombineWaves * 64) void combine_kernel(
+    const u32x4* __restrict__ eo, const int32_t* __restrict__ pos, const float* __restrict__ gates,
+    int64_t T, int K, int64_t nch, int64_t TK, u32x4* __restrict__ y, float* __restrict__ y32) {
+    const int64_t t = (int64_t)blockIdx.x * kCombineWaves + (threadIdx.x >> 6);
+    if (t >= T) return;
+    const int lane = threadIdx.x & 63;
+    int64_t row[kMaxK];
+    float g[kMaxK];
+    bool ok[kMaxK];
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+        ok[j] = false;
+        row[j] = 0;
+        g[j] = 0.f;
+        if (j < K) {
+            const int p = __builtin_amdgcn_readfirstlane(pos[t * K + j]);
+            ok[j] = p >= 0 && p < TK;
+            row[j] = (int64_t)p * nch;
+            g[j] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                                                  __builtin_bit_cast(int, gates[t * K + j])));
+        }
+    }
+    u32x4* yrow = y + t * nch;
+    for (int64_t c = lane; c < nch; c += 64) {
+        u32x4 v[kMaxK];
+#pragma unroll
+        for (int j = 0; j < kMaxK; ++j)
+            if (ok[j]) v[j] = __builtin_nontemporal_load(eo + row[j] + c);
+        float acc[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+#pragma unroll
+        for (int j = 0; j < kMaxK; ++j) {
+            if (!ok[j]) continue;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float lo = __uint_as_float(v[j][q] << 16);
+                const float hi = __uint_as_float(v[j][q] & 0xffff0000u);
+                acc[2 * q] = __builtin_fmaf(g[j], lo, acc[2 * q]);
+                acc[2 * q + 1] = __builtin_fmaf(g[j], hi, acc[2 * q + 1]);
+            }
+        }
+        u32x4 out;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            out[q] = f32_to_bf16_rne(acc[2 * q]) | (f32_to_bf16_rne(acc[2 * q + 1]) << 16);
+        __builtin_nontemporal_store(out, yrow + c);
+        if (kF32) {
+            float4* o = (float4*)(y32 + (t * nch + c) * 8);
+            o[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+            o[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+        }
+    }
+}
+
+}  // namespace
+
+cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* gates, int64_t T,
+                             int K, int64_t d, void* y, float* y32, hipStream_t s) {
+    const int64_t nch = d / 8;
+    const dim3 grid((unsigned)((T + kCombineWaves - 1) / kCombineWaves));
+    if (y32)
+        hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(kCombineWaves * 64), 0, s,
+                           (const u32x4*)eo, pos, gates, T, K, nch, T * K, (u32x4*)y, y32);
+    else
+        hipLaunchKernelGGL(combine_kernel<false>, grid, dim3(kCombineWaves * 64), 0, s,
+                           (const u32x4*)eo, pos, gates, T, K, nch, T * K, (u32x4*)y, y32);
+    COBALT_LAUNCH_CHECK();
+    return COBALT_OK;
+}
+
+// ---------------------------------------------------------------- validation
+
+namespace {
+
+__global__ void zero_flag_kernel(uint32_t* f) { *f = 0; }
+
+__global__ __launch_bounds__(256) void validate_kernel(const int32_t* __restrict__ topk,
+                                                       const int32_t* __restrict__ src, int64_t T,
+                                                       int K, int E, int G, uint32_t* flags) {
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= T) return;
+    uint32_t f = 0;
+    for (int j = 0; j < K; ++j) {
+        const int e = topk[t * K + j];
+        if (e < 0 || e >= E) f |= 1u;
+        for (int i = 0; i < j; ++i)
+            if (topk[t * K + i] == e) f |= 2u;
+    }
+    if (src) {
+        const int s = src[t];
+        if (s < 0 || s >= G) f |= 4u;
+        if (t > 0 && src[t - 1] > s) f |= 8u;
+    }
+    if (f) atomicOr(flags, f);
+}
+
+}  // namespace
+
+cobalt_status launch_validate(const int32_t* topk, const int32_t* src, int64_t T, int K, int E,
+                              int G, uint32_t* dflags, hipStream_t s) {
+    hipLaunchKernelGGL(zero_flag_kernel, dim3(1), dim3(1), 0, s, dflags);
+    COBALT_LAUNCH_CHECK();
+    hipLaunchKernelGGL(validate_kernel, dim3((unsigned)((T + 255) / 256)), dim3(256), 0, s, topk,
+                       src, T, K, E, G, dflags);
+    COBALT_LAUNCH_CHECK();
+    return COBALT_OK;
+}
+
+}  // namespace cobalt

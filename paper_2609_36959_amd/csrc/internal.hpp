@@ -1,0 +1,68 @@
+// Internal declarations of the HIP routing library (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "cobalt.h"
+
+namespace cobalt {
+
+constexpr int kMaxN = 16;
+constexpr int kMaxGpn = 32;
+constexpr int kMaxG = 512;
+constexpr int kMaxK = 16;
+constexpr int kMaxE = 4096;
+
+// 16-byte vector: eight bf16 values, the unit of every row copy.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+struct DeviceLayout {
+    int device;
+    int32_t N, g, G, E, S;
+    int32_t ncand;             // 2^(N-1) candidate covers
+    uint32_t* node_mask;       // [E]
+    uint32_t* rank_mask;       // [E][N]
+    int32_t* owner;            // [E]
+    uint16_t* cand;            // [ncand] remote-node masks by (popcount, value)
+};
+
+#define COBALT_LAUNCH_CHECK()                                        \
+    do {                                                             \
+        if (hipGetLastError() != hipSuccess) return COBALT_EHIP;     \
+    } while (0)
+
+// Per-device properties used to size launches.
+struct DeviceInfo {
+    int cus;
+    int lds_bytes;  // usable LDS per workgroup
+};
+cobalt_status device_info(DeviceInfo* out);
+
+// Launchers (argument checks are done by the C entry points).
+cobalt_status launch_coact_stats(const int32_t* topk, int64_t T, int K, int E, uint32_t* coact,
+                                 uint32_t* count, hipStream_t s);
+cobalt_status launch_assign(const DeviceLayout& L, const int32_t* topk, const int32_t* src,
+                            int64_t T, int K, uint64_t key, int mode, int32_t* out,
+                            uint16_t* remote, hipStream_t s);
+size_t dispatch_workspace_bytes(int64_t T, int K, int G);
+cobalt_status launch_dispatch(const int32_t* assigned, const int32_t* src, int64_t T, int K,
+                              int G, const void* x, int64_t d, int32_t* counts,
+                              int64_t* offsets, int32_t* pos, void* packed, void* ws,
+                              hipStream_t s);
+cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* gates, int64_t T,
+                             int K, int64_t d, void* y, float* y32, hipStream_t s);
+cobalt_status launch_validate(const int32_t* topk, const int32_t* src, int64_t T, int K, int E,
+                              int G, uint32_t* dflags, hipStream_t s);
+
+// SplitMix64 (Steele, Lea & Flood 2014): output of the generator for state z.
+__host__ __device__ inline uint64_t splitmix64(uint64_t z) {
+    z += 0x9e3779b97f4a7c15ull;
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    return z ^ (z >> 31);
+}
+
+}  // namespace cobalt

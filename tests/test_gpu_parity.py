@@ -1,0 +1,265 @@
+"""GPU parity: every step of the HIP path, called through the C ABI, against
+the oracle on the same seeded inputs, element by element. Sizes span
+several tiles with ragged tails; edge cases cover empty inputs, K = 1, one
+node, 16 nodes, tiny and long rows, and row bands of the statistics
+histogram."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_36959_amd import binding as B
+from paper_2609_36959_amd import pipeline as PL
+from paper_2609_36959_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    torch.cuda.set_device(0)
+    B.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def u32(t):
+    return t.cpu().numpy().view(np.uint32)
+
+
+def dev_i32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.int32)).cuda()
+
+
+def bits_to_bf16(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.uint16).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def run_path(w, seed, topk, gates, table, owner, src=None, x_bits=None, eo_bits=None, step=0,
+             mode=0, repeat=1):
+    """Runs the four calls on the GPU; returns host copies of every output."""
+    T, K, E, G, d = topk.shape[0], w.K, w.E, w.G, w.d
+    L = B.cobalt_layout_create(w.N, w.g, E, table.shape[1], table, owner)
+    t_topk = dev_i32(topk)
+    t_src = None if src is None else dev_i32(src)
+    coact = torch.zeros(E, E, dtype=torch.int32, device="cuda")
+    count = torch.zeros(E, dtype=torch.int32, device="cuda")
+    B.cobalt_coact_stats(t_topk, E, coact, count)
+    assigned = torch.full((T, K), -7, dtype=torch.int32, device="cuda")
+    remote = torch.zeros(T, dtype=torch.int16, device="cuda")
+    B.cobalt_assign(L, t_topk, t_src, seed, step, mode, assigned, remote)
+    x = bits_to_bf16(x_bits)
+    counts = torch.full((G, G), -1, dtype=torch.int32, device="cuda")
+    offsets = torch.full((G * G + 1,), -1, dtype=torch.int64, device="cuda")
+    pos = torch.full((T, K), -1, dtype=torch.int32, device="cuda")
+    packed = torch.zeros(T * K, d, dtype=torch.bfloat16, device="cuda")
+    ws = B.workspace_for(T, K, G)
+    ws.fill_(0xAB)  # contents on entry must not matter
+    outs = []
+    for _ in range(repeat):
+        B.cobalt_dispatch_pack(assigned, t_src, G, x, counts, offsets, pos, packed, ws)
+        outs.append((counts.cpu().numpy(), offsets.cpu().numpy(), pos.cpu().numpy(),
+                     PL.bf16_bits(packed)))
+    eo = bits_to_bf16(eo_bits)
+    y = torch.zeros(T, d, dtype=torch.bfloat16, device="cuda")
+    y32 = torch.zeros(T, d, dtype=torch.float32, device="cuda")
+    B.cobalt_combine(eo, pos, dev_gates(gates), y, y32)
+    torch.cuda.synchronize()
+    res = dict(coact=u32(coact), count=u32(count), assigned=assigned.cpu().numpy(),
+               remote=remote.cpu().numpy().view(np.uint16), dispatch=outs,
+               y=PL.bf16_bits(y), y32=y32.cpu().numpy(), tables=B.cobalt_layout_tables(L))
+    B.cobalt_layout_destroy(L)
+    return res
+
+
+def dev_gates(g):
+    return torch.from_numpy(np.ascontiguousarray(g, np.float32)).cuda()
+
+
+def check_against_oracle(w, seed, topk, gates, table, owner, src=None, step=0, mode=0, repeat=1):
+    T, K, E, G, d = topk.shape[0], w.K, w.E, w.G, w.d
+    gen = torch.Generator().manual_seed(seed + 17)
+    x_bits = PL.bf16_bits(torch.randn(T, d, generator=gen).to(torch.bfloat16))
+    eo_bits = PL.bf16_bits(torch.randn(T * K, d, generator=gen).to(torch.bfloat16))
+    got = run_path(w, seed, topk, gates, table, owner, src, x_bits, eo_bits, step, mode, repeat)
+
+    tabs = oracle.layout_tables(w.N, w.g, E, table, owner)
+    for mine, ref in zip(got["tables"], tabs):
+        assert np.array_equal(mine.view(ref.dtype), ref)
+    C, cnt = oracle.coact_stats(topk, E)
+    assert np.array_equal(got["coact"], C)
+    assert np.array_equal(got["count"], cnt)
+    a, rn = oracle.assign(w.N, w.g, E, tabs, topk, src, seed=seed, step=step, mode=mode)
+    assert np.array_equal(got["assigned"], a)
+    assert np.array_equal(got["remote"], rn)
+    counts, offsets, pos, packed = oracle.dispatch(a, G, src, x_bits)
+    for c2, o2, p2, pk2 in got["dispatch"]:
+        assert np.array_equal(c2, counts)
+        assert np.array_equal(o2, offsets)
+        assert np.array_equal(p2, pos)
+        assert np.array_equal(pk2, packed)
+    y, y32 = oracle.combine(eo_bits, pos, gates)
+    # acceptance bar: fp32 sums within 1e-3 of the oracle's, relative to the
+    # magnitude of the terms; the kernel keeps the oracle's order, so the
+    # results are in fact identical bit for bit
+    v = torch.from_numpy(eo_bits.view(np.int16)).view(torch.bfloat16).double().numpy()[pos]
+    scale = (np.abs(gates.astype(np.float64))[:, :, None] * np.abs(v)).sum(1)
+    assert np.all(np.abs(got["y32"].astype(np.float64) - y32) <= 1e-3 * scale + 1e-30)
+    assert np.array_equal(got["y32"].view(np.uint32), y32.view(np.uint32))
+    assert np.array_equal(got["y"], y)
+    return got
+
+
+CASES = [
+    # cfg, T, d, source ranks
+    (0, 4096, 512, "null"),
+    (0, 4096 + 8 * 37, 512, "null"),
+    (0, 3001, 128, "ragged"),
+    (1, 32 * 200, 2048, "null"),
+    (1, 5003, 256, "ragged"),
+    (2, 32 * 130, 4096, "null"),
+    (3, 64 * 40, 7168, "null"),
+    (3, 2999, 64, "ragged"),
+    (4, 64 * 33, 1024, "null"),
+]
+
+
+@pytest.mark.parametrize("cfg,T,d,srckind", CASES)
+@pytest.mark.parametrize("mode", [0, 1])
+def test_path_matches_oracle(cfg, T, d, srckind, mode):
+    w = W.with_sizes(W.CONFIGS[cfg], T=T, d=d)
+    print(f"case cfg={cfg} T={T} d={d} src={srckind} mode={mode}", flush=True)
+    topk, gates = W.routing(w, cfg)
+    table, owner = W.layout(w, cfg)
+    src = None if srckind == "null" else W.ragged_src(T, w.G, seed=cfg)
+    check_against_oracle(w, cfg, topk.numpy(), gates.numpy(), table, owner, src, step=3,
+                         mode=mode)
+
+
+def test_deterministic_repeats_and_stale_workspace():
+    w = W.with_sizes(W.CONFIGS[3], T=64 * 70, d=256)
+    topk, gates = W.routing(w, 5)
+    table, owner = W.layout(w, 5)
+    got = check_against_oracle(w, 5, topk.numpy(), gates.numpy(), table, owner, repeat=4)
+    first = got["dispatch"][0]
+    for other in got["dispatch"][1:]:
+        for a, b in zip(first, other):
+            assert np.array_equal(a, b)
+
+
+def test_statistics_accumulate_across_calls():
+    w = W.with_sizes(W.CONFIGS[4], T=64 * 40)
+    E = w.E
+    coact = torch.zeros(E, E, dtype=torch.int32, device="cuda")
+    count = torch.zeros(E, dtype=torch.int32, device="cuda")
+    C = np.zeros((E, E), np.uint32)
+    cnt = np.zeros(E, np.uint32)
+    for step in range(3):
+        topk, _ = W.routing(w, 4, step=step)
+        B.cobalt_coact_stats(topk.cuda(), E, coact, count)
+        C, cnt = oracle.coact_stats(topk.numpy(), E, C, cnt)
+    torch.cuda.synchronize()
+    assert np.array_equal(u32(coact), C) and np.array_equal(u32(count), cnt)
+
+
+@pytest.mark.parametrize("E", [384, 1024, 2])
+def test_statistics_row_bands(E):
+    """E = 384 and 1024 need several LDS row bands of the pair triangle."""
+    rng = np.random.default_rng(E)
+    T, K = 3000, 8 if E > 8 else 2
+    topk = np.stack([rng.choice(E, size=K, replace=False) for _ in range(T)]).astype(np.int32)
+    coact = torch.zeros(E, E, dtype=torch.int32, device="cuda")
+    B.cobalt_coact_stats(dev_i32(topk), E, coact, None)
+    C, _ = oracle.coact_stats(topk, E)
+    assert np.array_equal(u32(coact), C)
+
+
+def _custom(N, g, E, S, K, T, d, seed, extra_per_rank=None):
+    w = W.Workload("custom", T, E, K, d, N, g, S)
+    rng = np.random.default_rng(seed)
+    G = N * g
+    per = E // G
+    slots = [list(range(r * per, (r + 1) * per)) for r in range(G)]
+    for e in rng.permutation(E):
+        cand = [r for r in range(G) if len(slots[r]) < S and e not in slots[r]]
+        if cand and rng.random() < 0.7:
+            slots[cand[rng.integers(len(cand))]].append(int(e))
+    table = np.full((G, S), -1, np.int32)
+    for r in range(G):
+        table[r, : len(slots[r])] = slots[r]
+    owner = (np.arange(E) // per).astype(np.int32)
+    topk = np.stack([rng.choice(E, size=K, replace=False) for _ in range(T)]).astype(np.int32)
+    g_ = rng.random((T, K)).astype(np.float32)
+    gates = (g_ / g_.sum(1, keepdims=True)).astype(np.float32)
+    return w, topk, gates, table, owner
+
+
+@pytest.mark.parametrize("N,g,E,S,K,T,d", [
+    (1, 4, 16, 6, 3, 4 * 301, 64),      # one node: nothing remote
+    (16, 2, 64, 4, 8, 32 * 41, 32),     # 16 nodes: 15-bit remote masks
+    (4, 8, 64, 3, 1, 32 * 50, 8),       # K = 1 and one-vector rows
+    (2, 4, 16, 4, 16, 8 * 90, 8200),    # K = 16; rows of 1025 vectors (long copy path)
+    (8, 1, 8, 3, 4, 8 * 100, 16),       # one GPU per node
+])
+def test_edge_shapes(N, g, E, S, K, T, d):
+    w, topk, gates, table, owner = _custom(N, g, E, S, K, T, d, seed=N * 100 + K)
+    check_against_oracle(w, 9, topk, gates, table, owner, step=1)
+    check_against_oracle(w, 9, topk, gates, table, owner, step=1, mode=1)
+
+
+def test_empty_inputs_are_no_ops():
+    w = W.CONFIGS[0]
+    table, owner = W.layout(w, 0)
+    L = B.cobalt_layout_create(w.N, w.g, w.E, w.S, table, owner)
+    e0 = torch.zeros(0, w.K, dtype=torch.int32, device="cuda")
+    coact = torch.zeros(w.E, w.E, dtype=torch.int32, device="cuda")
+    B.cobalt_coact_stats(e0, w.E, coact)
+    B.cobalt_assign(L, e0, None, 0, 0, 0, e0.clone())
+    counts = torch.full((w.G, w.G), 5, dtype=torch.int32, device="cuda")
+    offsets = torch.full((w.G * w.G + 1,), 5, dtype=torch.int64, device="cuda")
+    x0 = torch.zeros(0, 64, dtype=torch.bfloat16, device="cuda")
+    p0 = torch.zeros(0, 64, dtype=torch.bfloat16, device="cuda")
+    B.cobalt_dispatch_pack(e0, None, w.G, x0, counts, offsets, e0.clone(), p0,
+                           B.workspace_for(0, w.K, w.G))
+    B.cobalt_combine(p0, e0, torch.zeros(0, w.K, device="cuda"), x0.clone())
+    torch.cuda.synchronize()
+    assert int(coact.abs().sum()) == 0
+    assert int(counts.abs().sum()) == 0 and int(offsets.abs().sum()) == 0
+    B.cobalt_layout_destroy(L)
+
+
+def test_index_only_dispatch_matches():
+    w = W.with_sizes(W.CONFIGS[1], T=32 * 77)
+    topk, _ = W.routing(w, 1)
+    table, owner = W.layout(w, 1)
+    L = B.cobalt_layout_create(w.N, w.g, w.E, w.S, table, owner)
+    a = torch.empty(w.T, w.K, dtype=torch.int32, device="cuda")
+    B.cobalt_assign(L, topk.cuda(), None, 1, 0, 0, a)
+    counts = torch.empty(w.G, w.G, dtype=torch.int32, device="cuda")
+    offsets = torch.empty(w.G * w.G + 1, dtype=torch.int64, device="cuda")
+    pos = torch.empty(w.T, w.K, dtype=torch.int32, device="cuda")
+    B.cobalt_dispatch_pack(a, None, w.G, None, counts, offsets, pos, None,
+                           B.workspace_for(w.T, w.K, w.G))
+    c, o, p, _ = oracle.dispatch(a.cpu().numpy(), w.G)
+    assert np.array_equal(pos.cpu().numpy(), p) and np.array_equal(offsets.cpu().numpy(), o)
+    B.cobalt_layout_destroy(L)
+
+
+def test_validate_routing_flags():
+    topk = dev_i32([[0, 1], [2, 2], [3, 9]])
+    assert B.cobalt_validate_routing(topk, None, 4, 4) == 1 | 2
+    src = dev_i32([0, 2, 1])
+    assert B.cobalt_validate_routing(topk, src, 16, 4) & 8
+    assert B.cobalt_validate_routing(dev_i32([[0, 1], [2, 3]]), dev_i32([0, 3]), 4, 4) == 0
+    assert B.cobalt_validate_routing(dev_i32([[0, 1]]), dev_i32([4]), 4, 4) == 4
+
+
+def test_round_trip_returns_x():
+    """expert_out = packed, gates summing to one: y equals x by value."""
+    w = W.with_sizes(W.CONFIGS[2], T=32 * 64, d=1024)
+    st = PL.RoutingStep(w, seed=2, device="cuda", expert_out="roundtrip", route_device="cpu")
+    st.run()
+    torch.cuda.synchronize()
+    assert torch.equal(st.y.float(), st.x.float())
+    st.close()
