@@ -1,0 +1,247 @@
+"""Benchmark of the co-activation routing path on one MI355X.
+
+One step = one pass of the whole path over one batch: co-activation
+statistics, communication-aware assignment (Algorithm 1), dispatch layout +
+pack, and the gate-weighted combine, on the workload with T=131072 tokens,
+E=256 experts, top-8, d=7168 bf16, 8 virtual nodes x 8 GPUs, 5 slots per
+GPU (co-located planted clusters, Zipf-skewed popularity). Inputs are
+seeded synthetic data resident in HBM before timing starts.
+
+Prints one JSON line: routed tokens/s over the timed steps, the roofline
+position of the dominant call, the pack+combine share of HBM peak, routing
+quality (cross-node traffic of Algorithm 1 vs owner-only baselines), and the
+oracle's CPU throughput on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--config C] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12  # MI355X HBM3E, bytes/s
+METRIC = "routed tokens/sec (stats+assign+pack+combine), % of HBM peak, 1 MI355X"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_{call}_{workload}.txt")
+KERNEL_SOURCES = {"cobalt_dispatch_pack": "dispatch.hip", "cobalt_combine": "combine.hip"}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=16384)
+    return ap.parse_args()
+
+
+def algorithmic_bytes(w):
+    """Bytes each call must move (read + write), per call (one step)."""
+    T, K, d, E, G = w.T, w.K, w.d, w.E, w.G
+    return {
+        "cobalt_coact_stats": T * K * 4 + 2 * 4 * (E * E + E),
+        "cobalt_assign": T * K * 4 + T * K * 4 + T * 2,
+        "cobalt_dispatch_pack": T * d * 2 + T * K * d * 2 + T * K * 8 + 12 * G * G,
+        "cobalt_combine": T * K * d * 2 + T * K * 8 + T * d * 2,
+    }
+
+
+def source_digest(call):
+    p = os.path.join(ROOT, "paper_2609_36959_amd", "csrc", KERNEL_SOURCES[call])
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(call, workload):
+    """HBM bytes per call from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source; else None."""
+    p = TRAFFIC_FILE.format(call=call, workload=workload)
+    if not os.path.exists(p):
+        return None
+    kv = {}
+    for line in open(p):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256_16") != source_digest(call):
+        return None
+    try:
+        return float(kv["hbm_bytes_per_call"])
+    except (KeyError, ValueError):
+        return None
+
+
+def routing_quality(st, torch, B, W):
+    """Cross-node traffic (Eq. 1) of Algorithm 1 against two owner-only
+    baselines: on the same layout, and on plain contiguous expert parallelism
+    without replicas. Reporting only (outside the timed region)."""
+    w = st.w
+
+    def measure(layout, mode):
+        a = torch.empty_like(st.assigned)
+        rn = torch.empty_like(st.remote)
+        B.cobalt_assign(layout, st.topk, None, st.seed, 0, mode, a, rn)
+        torch.cuda.synchronize()
+        src_node = (torch.arange(w.T, device=a.device) // (w.T // w.G)) // w.g
+        cross = (a // w.g != src_node[:, None]).sum().item()
+        rn32 = rn.to(torch.int32) & 0xFFFF
+        V = sum(((rn32 >> n) & 1).sum().item() for n in range(w.N))
+        load = torch.bincount(a.flatten(), minlength=w.G).float()
+        return {"V": int(V), "cross_pair_frac": cross / (w.T * w.K),
+                "imbalance": float(load.max() / load.mean())}
+
+    out = {"alg1": measure(st.layout, 0), "owner_only": measure(st.layout, 1)}
+    t, o = W.contiguous_ep_layout(w)
+    L = B.cobalt_layout_create(w.N, w.g, w.E, t.shape[1], t, o)
+    out["contiguous_ep_owner_only"] = measure(L, 1)
+    B.cobalt_layout_destroy(L)
+    for k in ("owner_only", "contiguous_ep_owner_only"):
+        base = out[k]["V"]
+        out[f"V_reduction_vs_{k}"] = 1.0 - out["alg1"]["V"] / base if base else 0.0
+    return out
+
+
+def cpu_baseline(st, n_tokens, torch, W, PL):
+    """The oracle, as it stands, on the first n_tokens of the same workload,
+    in chunks of 4096 tokens (each chunk a full pass: stats, assign, dispatch
+    with packed rows, combine). Single-threaded C."""
+    import numpy as np
+
+    import oracle
+
+    w = st.w
+    tabs = oracle.layout_tables(w.N, w.g, w.E, st.table, st.owner)
+    src_all = W.contiguous_src(w.T, w.G)
+    chunk = 4096
+    n_tokens = min(n_tokens, w.T)
+    total = 0.0
+    done = 0
+    for t0 in range(0, n_tokens, chunk):
+        n = min(chunk, n_tokens - t0)
+        topk = st.topk[t0:t0 + n].cpu().numpy()
+        gates = st.gates[t0:t0 + n].cpu().numpy()
+        src = np.ascontiguousarray(src_all[t0:t0 + n])
+        x = PL.bf16_bits(st.x[t0:t0 + n])
+        eo = PL.bf16_bits(st.eo[t0 * w.K:(t0 + n) * w.K])
+        c0 = time.perf_counter()
+        oracle.coact_stats(topk, w.E)
+        a, _ = oracle.assign(w.N, w.g, w.E, tabs, topk, src, seed=st.seed, step=0)
+        _, _, pos, _ = oracle.dispatch(a, w.G, src, x)
+        oracle.combine(eo, pos, gates)
+        total += time.perf_counter() - c0
+        done += n
+    return {"value": done / total, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {done} tokens of the same workload in chunks of {chunk} "
+                      f"(stats, assign, dispatch with packed rows, combine), "
+                      f"{total:.1f} s on one host core"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path has "
+              "no inter-GPU collectives in this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2609_36959_amd import binding as B
+    from paper_2609_36959_amd import pipeline as PL
+    from paper_2609_36959_amd import workload as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    B.lib()
+    w = W.CONFIGS[args.config]
+    if w.steps > 1:
+        print("note: timing one step of the drift workload", file=sys.stderr)
+    seed = args.config if args.seed is None else args.seed
+    wl_name = f"t{w.T}_e{w.E}_k{w.K}_d{w.d}"
+    st = PL.RoutingStep(w, seed=seed, device="cuda", expert_out="independent")
+    stream = torch.cuda.Stream()
+    calls = ["cobalt_coact_stats", "cobalt_assign", "cobalt_dispatch_pack", "cobalt_combine"]
+    fns = [st.stats, st.assign, st.pack, st.combine]
+
+    # a plain copy of known size, the reference for HBM counter readings
+    calib = torch.empty(1 << 28, dtype=torch.int32, device="cuda")  # 1 GiB
+    calib_dst = torch.empty_like(calib)
+    with torch.cuda.stream(stream):
+        calib_dst.copy_(calib)
+    torch.cuda.synchronize()
+    del calib, calib_dst
+
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            for f in fns:
+                f(stream=stream)
+    torch.cuda.synchronize()
+    assert int(st.offsets[-1].item()) == w.T * w.K, "dispatch placed the wrong number of rows"
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)]
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    with torch.cuda.stream(stream):
+        for k in range(args.steps):
+            e = evs[k]
+            e[0].record(stream)
+            for i, f in enumerate(fns):
+                f(stream=stream)
+                e[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    call_ms = {c: 0.0 for c in calls}
+    for e in evs:
+        for i, c in enumerate(calls):
+            call_ms[c] += e[i].elapsed_time(e[i + 1]) / args.steps
+    ab = algorithmic_bytes(w)
+    dominant = max(("cobalt_dispatch_pack", "cobalt_combine"), key=lambda c: call_ms[c])
+    achieved = ab[dominant] / (call_ms[dominant] * 1e-3)
+    traffic = measured_traffic(dominant, wl_name)
+    pc_bytes = ab["cobalt_dispatch_pack"] + ab["cobalt_combine"]
+    pc_s = (call_ms["cobalt_dispatch_pack"] + call_ms["cobalt_combine"]) * 1e-3
+    step_bytes = sum(ab.values())
+
+    result = {
+        "metric": METRIC,
+        "value": w.T * args.steps / wall,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"co-activation routing step, {w.describe()}, "
+                               f"{w.name}, seed {seed}",
+                   "T": w.T, "E": w.E, "K": w.K, "d": w.d, "nodes": w.N,
+                   "gpus_per_node": w.g, "slots_per_gpu": w.S,
+                   "parallelism": "single GPU; virtual ranks are HBM buffers"},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved / 1e9,
+                     "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": achieved / HBM_PEAK,
+                     "traffic": traffic},
+        "pack_combine_hbm_frac": pc_bytes / pc_s / HBM_PEAK,
+        "step_hbm_frac": step_bytes / (wall / args.steps) / HBM_PEAK,
+        "call_ms": call_ms,
+        "call_gbps": {c: ab[c] / (call_ms[c] * 1e-3) / 1e9 for c in calls},
+    }
+    result["routing"] = routing_quality(st, torch, B, W)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(st, args.cpu_sample_tokens, torch, W, PL)
+    st.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
