@@ -40,7 +40,7 @@ def parse():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=16384)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=65536)
     return ap.parse_args()
 
 
@@ -169,11 +169,12 @@ def main():
     calls = ["cobalt_coact_stats", "cobalt_assign", "cobalt_dispatch_pack", "cobalt_combine"]
     fns = [st.stats, st.assign, st.pack, st.combine]
 
-    # a plain copy of known size, the reference for HBM counter readings
-    calib = torch.empty(1 << 28, dtype=torch.int32, device="cuda")  # 1 GiB
+    # a streaming kernel of known size (reads 1 GiB, writes 1 GiB), the
+    # reference against which HBM counter readings are scaled
+    calib = torch.zeros(1 << 28, dtype=torch.int32, device="cuda")
     calib_dst = torch.empty_like(calib)
     with torch.cuda.stream(stream):
-        calib_dst.copy_(calib)
+        torch.bitwise_not(calib, out=calib_dst)
     torch.cuda.synchronize()
     del calib, calib_dst
 

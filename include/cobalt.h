@@ -62,10 +62,10 @@ const char* cobalt_status_string(cobalt_status s);
  * rule of Section 3.2, Stage 2), an owner does not hold its expert, or an
  * id lies outside [-1, E). The slot budget S = (1+rho)E/G of Eq. 2 is the
  * table's width.
- * Derives node_mask[e] (bit n: e on node n), rank_mask[e][n] (bit i: e on
- * rank n*g+i) and the candidate-cover order used by cobalt_assign, and
- * copies them to the current device. Synchronous; the handle belongs to
- * the device current at creation and may only be used there.
+ * Derives node_mask[e] (bit n: e on node n) and rank_mask[e][n] (bit i: e
+ * on rank n*g+i) and copies them, with the owners, to the current device.
+ * Synchronous; the handle belongs to the device current at creation and may
+ * only be used there.
  * ---------------------------------------------------------------------- */
 typedef struct cobalt_layout_s* cobalt_layout_t;
 
@@ -92,9 +92,18 @@ cobalt_status cobalt_layout_tables(cobalt_layout_t layout, uint32_t* host_node_m
  * across calls (and steps) until the caller clears them. With distinct
  * experts per token coact is symmetric with a zero diagonal and row sums
  * (K-1) * expert_count.
+ * workspace: device scratch of at least cobalt_coact_stats_workspace_bytes(
+ *   T, K, E) bytes (partial histograms, about 4 * min(64, T/2048) * E(E-1)/2
+ *   bytes), 256-byte aligned, owned by the caller; contents on entry are
+ *   ignored; it must not be shared by calls that may overlap. The call
+ *   updates coact and expert_count with plain (non-atomic) adds, so calls
+ *   that may overlap must not share them either.
  * ---------------------------------------------------------------------- */
+size_t cobalt_coact_stats_workspace_bytes(int64_t T, int32_t K, int32_t E);
+
 cobalt_status cobalt_coact_stats(const int32_t* topk_idx, int64_t T, int32_t K, int32_t E,
-                                 uint32_t* coact, uint32_t* expert_count, void* stream);
+                                 uint32_t* coact, uint32_t* expert_count,
+                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Step 2: communication-aware task assignment (Section 3.3, Algorithm 1).

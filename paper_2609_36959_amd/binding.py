@@ -53,7 +53,8 @@ def lib() -> ctypes.CDLL:
         "cobalt_layout_create": ([i32, i32, i32, i32, P, P, ctypes.POINTER(P)], ctypes.c_int),
         "cobalt_layout_destroy": ([P], ctypes.c_int),
         "cobalt_layout_tables": ([P, P, P, P], ctypes.c_int),
-        "cobalt_coact_stats": ([P, i64, i32, i32, P, P, P], ctypes.c_int),
+        "cobalt_coact_stats_workspace_bytes": ([i64, i32, i32], sz),
+        "cobalt_coact_stats": ([P, i64, i32, i32, P, P, P, sz, P], ctypes.c_int),
         "cobalt_assign": ([P, P, P, i64, i32, u64, u64, i32, P, P, P], ctypes.c_int),
         "cobalt_dispatch_workspace_bytes": ([i64, i32, i32], sz),
         "cobalt_dispatch_pack": ([P, P, i64, i32, i32, P, i64, P, P, P, P, P, sz, P],
@@ -100,6 +101,7 @@ U16 = (torch.int16, torch.uint16)
 BF16 = (torch.bfloat16,)
 F32 = (torch.float32,)
 I64 = (torch.int64,)
+WS = (torch.uint8, torch.int8, torch.int32, torch.int64)
 
 
 # ------------------------------------------------------------------- layout
@@ -146,11 +148,17 @@ def cobalt_layout_tables(layout: Layout):
 
 
 # ---------------------------------------------------------------- path calls
+def cobalt_coact_stats_workspace_bytes(T: int, K: int, E: int) -> int:
+    return int(lib().cobalt_coact_stats_workspace_bytes(T, K, E))
+
+
 def cobalt_coact_stats(topk_idx: torch.Tensor, E: int, coact: torch.Tensor,
-                       expert_count: Optional[torch.Tensor] = None, stream=None) -> None:
+                       expert_count: Optional[torch.Tensor], workspace: torch.Tensor,
+                       stream=None) -> None:
     T, K = topk_idx.shape
     _call("cobalt_coact_stats", _dev(topk_idx, "topk_idx", I32), T, K, E,
           _dev(coact, "coact", U32, (E, E)), _dev(expert_count, "expert_count", U32, (E,)),
+          _dev(workspace, "workspace", WS), workspace.numel() * workspace.element_size(),
           _stream(stream))
 
 
@@ -183,7 +191,7 @@ def cobalt_dispatch_pack(assigned_rank: torch.Tensor, src_rank: Optional[torch.T
           _dev(send_offsets, "send_offsets", I64, (G * G + 1,)),
           _dev(pos, "pos", I32, (T, K)),
           _dev(packed, "packed", BF16, None if packed is None else (T * K, d)),
-          _dev(workspace, "workspace", (torch.uint8, torch.int8, torch.int32, torch.int64)),
+          _dev(workspace, "workspace", WS),
           workspace.numel() * workspace.element_size(), _stream(stream))
 
 
@@ -212,4 +220,10 @@ def cobalt_validate_routing(topk_idx: torch.Tensor, src_rank: Optional[torch.Ten
 def workspace_for(T: int, K: int, G: int, device="cuda") -> torch.Tensor:
     """A dispatch workspace of the size the library asks for."""
     n = cobalt_dispatch_workspace_bytes(T, K, G)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+
+
+def stats_workspace_for(T: int, K: int, E: int, device="cuda") -> torch.Tensor:
+    """A statistics workspace of the size the library asks for."""
+    n = cobalt_coact_stats_workspace_bytes(T, K, E)
     return torch.empty(max(n, 256), dtype=torch.uint8, device=device)

@@ -49,17 +49,13 @@ cobalt_status device_info(DeviceInfo* out) {
 
 }  // namespace cobalt
 
-static int popcount_u32(uint32_t v) { return __builtin_popcount(v); }
-
 static void free_layout(DeviceLayout& d) {
     (void)hipFree(d.node_mask);
     (void)hipFree(d.rank_mask);
     (void)hipFree(d.owner);
-    (void)hipFree(d.cand);
     d.node_mask = nullptr;
     d.rank_mask = nullptr;
     d.owner = nullptr;
-    d.cand = nullptr;
 }
 
 extern "C" cobalt_status cobalt_layout_create(int32_t N, int32_t gpn, int32_t E, int32_t S,
@@ -96,15 +92,6 @@ extern "C" cobalt_status cobalt_layout_create(int32_t N, int32_t gpn, int32_t E,
             owner[e] = o;
         }
     }
-    // Remote-node covers in the order Algorithm 1 prefers them: fewer nodes
-    // first, then the smaller bitmask.
-    const int32_t ncand = 1 << (N - 1);
-    std::vector<uint16_t> cand(ncand);
-    for (int32_t b = 0; b < ncand; ++b) cand[b] = (uint16_t)b;
-    std::stable_sort(cand.begin(), cand.end(), [](uint16_t a, uint16_t b) {
-        return popcount_u32(a) < popcount_u32(b);
-    });
-
     auto* L = new (std::nothrow) cobalt_layout_s();
     if (!L) return COBALT_ENOMEM;
     DeviceLayout& d = L->d;
@@ -117,11 +104,9 @@ extern "C" cobalt_status cobalt_layout_create(int32_t N, int32_t gpn, int32_t E,
     d.G = G;
     d.E = E;
     d.S = S;
-    d.ncand = ncand;
     if (hipMalloc(&d.node_mask, sizeof(uint32_t) * E) != hipSuccess ||
         hipMalloc(&d.rank_mask, sizeof(uint32_t) * E * N) != hipSuccess ||
-        hipMalloc(&d.owner, sizeof(int32_t) * E) != hipSuccess ||
-        hipMalloc(&d.cand, sizeof(uint16_t) * ncand) != hipSuccess) {
+        hipMalloc(&d.owner, sizeof(int32_t) * E) != hipSuccess) {
         free_layout(d);
         delete L;
         return COBALT_ENOMEM;
@@ -131,8 +116,6 @@ extern "C" cobalt_status cobalt_layout_create(int32_t N, int32_t gpn, int32_t E,
         hipMemcpy(d.rank_mask, rank_mask.data(), sizeof(uint32_t) * E * N,
                   hipMemcpyHostToDevice) != hipSuccess ||
         hipMemcpy(d.owner, owner.data(), sizeof(int32_t) * E, hipMemcpyHostToDevice) !=
-            hipSuccess ||
-        hipMemcpy(d.cand, cand.data(), sizeof(uint16_t) * ncand, hipMemcpyHostToDevice) !=
             hipSuccess) {
         free_layout(d);
         delete L;
@@ -178,13 +161,24 @@ extern "C" cobalt_status cobalt_layout_tables(cobalt_layout_t L, uint32_t* node_
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+extern "C" size_t cobalt_coact_stats_workspace_bytes(int64_t T, int32_t K, int32_t E) {
+    if (T < 0 || K < 1 || K > kMaxK || E < 1 || E > kMaxE) return 0;
+    // the larger of the plans for 64 KiB and 160 KiB of LDS per workgroup
+    return std::max<size_t>(std::max<size_t>(coact_workspace_bytes(T, E, 64 * 1024),
+                                             coact_workspace_bytes(T, E, 160 * 1024)),
+                            256);
+}
+
 extern "C" cobalt_status cobalt_coact_stats(const int32_t* topk, int64_t T, int32_t K, int32_t E,
-                                            uint32_t* coact, uint32_t* count, void* stream) {
-    if (T < 0 || K < 1 || K > kMaxK || E < 1 || E > kMaxE || !coact) return COBALT_EINVAL;
+                                            uint32_t* coact, uint32_t* count, void* ws,
+                                            size_t ws_bytes, void* stream) {
+    if (T < 0 || K < 1 || K > kMaxK || E < 1 || E > kMaxE || !coact || !ws) return COBALT_EINVAL;
     if (T > 0 && !topk) return COBALT_EINVAL;
+    if (((uintptr_t)ws & 255u) != 0) return COBALT_EINVAL;
     if (T * K >= (int64_t(1) << 31)) return COBALT_EUNSUPPORTED;
+    if (ws_bytes < cobalt_coact_stats_workspace_bytes(T, K, E)) return COBALT_EINVAL;
     if (T == 0) return COBALT_OK;
-    return launch_coact_stats(topk, T, K, E, coact, count, (hipStream_t)stream);
+    return launch_coact_stats(topk, T, K, E, coact, count, ws, ws_bytes, (hipStream_t)stream);
 }
 
 extern "C" cobalt_status cobalt_assign(cobalt_layout_t L, const int32_t* topk,

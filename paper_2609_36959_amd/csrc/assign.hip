@@ -2,14 +2,23 @@
 // per token.
 //
 // Step 1 (select execution nodes): the token's experts without a replica on
-// the source node form U_t, each with its remote-node mask (N-1 bits, bit i
-// = the i-th node other than the source node). The masks are packed into
-// SWAR words, one 8- or 16-bit lane per slot, and a candidate cover b is
-// tested for all slots at once: it is feasible iff no lane of
-// (packed & broadcast(b)) | fill is zero, where fill makes the lanes of
-// slots outside U_t non-zero. Candidates are tried in the layout's
-// (popcount, value) order and the first feasible one is the cover Algorithm 1
-// keeps. Each expert of U_t then draws one of the cover's nodes holding it.
+// the source node form U_t, each with its remote-node mask m (N-1 bits, bit
+// i = the i-th node other than the source node). Algorithm 1 keeps the first
+// feasible cover in order of (node count, mask value). The search here
+// reaches the same cover without a table:
+//  - F, the union of the masks with a single node, is contained in every
+//    feasible cover. If F meets every mask of U_t, no other cover has as few
+//    nodes, so F is the answer.
+//  - Otherwise the answer is F | S, where S is the first subset, by (size,
+//    value), of A = (union of the masks F misses) that meets each of those
+//    masks (nodes outside A can only be dropped). Subsets of A of size c are
+//    enumerated in increasing value with Gosper's next-combination step on
+//    c-bit patterns deposited onto the bits of A; since F and S are disjoint
+//    this is the order of F | S. The masks F misses are packed into SWAR
+//    words, one 8- or 16-bit lane per slot, so each subset is tested for all
+//    slots at once: it meets every mask iff no lane of
+//    (packed & broadcast(S)) | fill is zero.
+// Each expert of U_t then draws one of the cover's nodes holding it.
 // Step 2 (select execution ranks): every task draws one rank of its node
 // holding the expert. Draws hash the pair index with SplitMix64.
 #include "internal.hpp"
@@ -24,12 +33,11 @@ struct AssignArgs {
     const int32_t* src;
     int64_t T;
     int64_t tok_per_src;
-    int K, E, N, g, G, ncand, mode;
+    int K, E, N, g, G, mode;
     uint64_t key;
     const uint32_t* node_mask;
     const uint32_t* rank_mask;
     const int32_t* owner;
-    const uint16_t* cand;
     int32_t* out;
     uint16_t* remote;
 };
@@ -101,18 +109,9 @@ __global__ __launch_bounds__(kAssignThreads) void assign_kernel(AssignArgs a) {
         return;
     }
 
-    // Step 1: remote masks of U_t, packed one lane per slot.
-    // packed lane j = m_j for experts of U_t, 0 otherwise; fill lane j is
-    // non-zero exactly for the other slots, so (packed & b) | fill has a
-    // zero lane iff some expert of U_t has no node in b.
+    // Step 1: remote masks of U_t and the nodes every cover needs.
     uint32_t m[kMaxK];
-    uint64_t packed[SW::kWords], fill[SW::kWords];
-#pragma unroll
-    for (int w = 0; w < SW::kWords; ++w) {
-        packed[w] = 0;
-        fill[w] = SW::kOnes;
-    }
-    bool any_remote = false;
+    uint32_t forced = 0;
 #pragma unroll
     for (int j = 0; j < kMaxK; ++j) {
         m[j] = 0;
@@ -120,30 +119,60 @@ __global__ __launch_bounds__(kAssignThreads) void assign_kernel(AssignArgs a) {
             const uint32_t nm = a.node_mask[e[j]];
             if (!(nm & home_bit)) {
                 m[j] = (nm & low) | ((nm >> (home + 1)) << home);
-                const int w = j / SW::kLanes, sh = (j % SW::kLanes) * LB;
-                packed[w] |= (uint64_t)m[j] << sh;
-                fill[w] &= ~(SW::kLaneMask << sh);
-                any_remote = true;
+                if ((m[j] & (m[j] - 1u)) == 0) forced |= m[j];
             }
         }
     }
-    uint32_t bstar = 0;
-    if (any_remote) {
-        // The all-remote cover is feasible whenever every expert has a
-        // replica, so the scan always stops; the bound guards bad layouts.
-        bstar = (uint32_t)a.ncand - 1u;
-        for (int i = 0; i < a.ncand; ++i) {
-            const uint32_t b = a.cand[i];
-            const uint64_t bb = (uint64_t)b * SW::kOnes;
-            bool ok = true;
+    // Masks the forced nodes miss, packed one lane per slot; fill lane j is
+    // non-zero exactly for the other slots.
+    uint64_t packed[SW::kWords], fill[SW::kWords];
 #pragma unroll
-            for (int w = 0; w < SW::kWords; ++w)
-                ok = ok && !SW::has_zero_lane((packed[w] & bb) | fill[w]);
-            if (ok) {
-                bstar = b;
-                break;
+    for (int w = 0; w < SW::kWords; ++w) {
+        packed[w] = 0;
+        fill[w] = SW::kOnes;
+    }
+    uint32_t spare = 0;  // A: nodes that can still help
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+        if (m[j] && !(m[j] & forced)) {
+            const int w = j / SW::kLanes, sh = (j % SW::kLanes) * LB;
+            packed[w] |= (uint64_t)m[j] << sh;
+            fill[w] &= ~(SW::kLaneMask << sh);
+            spare |= m[j];
+        }
+    }
+    uint32_t bstar = forced;
+    if (spare) {
+        const int na = __builtin_popcount(spare);
+        uint32_t extra = spare;  // the whole of A always meets every mask
+        bool found = false;
+        for (int c = 1; c <= na && !found; ++c) {
+            for (uint32_t pat = (1u << c) - 1u; pat < (1u << na);) {
+                // deposit the bits of pat onto the set bits of A, in order
+                uint32_t sub = 0, rest = spare, pp = pat;
+                while (pp) {
+                    const uint32_t low_bit = rest & (0u - rest);
+                    if (pp & 1u) sub |= low_bit;
+                    rest ^= low_bit;
+                    pp >>= 1;
+                }
+                const uint64_t bb = (uint64_t)sub * SW::kOnes;
+                bool ok = true;
+#pragma unroll
+                for (int w = 0; w < SW::kWords; ++w)
+                    ok = ok && !SW::has_zero_lane((packed[w] & bb) | fill[w]);
+                if (ok) {
+                    extra = sub;
+                    found = true;
+                    break;
+                }
+                // Gosper's hack: next larger pattern with the same popcount
+                const uint32_t u = pat & (0u - pat);
+                const uint32_t v = pat + u;
+                pat = v + (((v ^ pat) >> __builtin_ctz(u)) >> 2);
             }
         }
+        bstar |= extra;
     }
 
     // Node of each task, then its rank (Step 2).
@@ -184,13 +213,11 @@ cobalt_status launch_assign(const DeviceLayout& L, const int32_t* topk, const in
     a.N = L.N;
     a.g = L.g;
     a.G = L.G;
-    a.ncand = L.ncand;
     a.mode = mode;
     a.key = key;
     a.node_mask = L.node_mask;
     a.rank_mask = L.rank_mask;
     a.owner = L.owner;
-    a.cand = L.cand;
     a.out = out;
     a.remote = remote;
     const unsigned blocks = (unsigned)((T + kAssignThreads - 1) / kAssignThreads);

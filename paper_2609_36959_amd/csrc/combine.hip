@@ -1,9 +1,11 @@
-// Combine and weighted sum (Fig. 1, last stage): one wave per token. Each
-// lane owns 16-byte column chunks of the output row; for a chunk it loads
-// the K expert-output chunks (pos[t][j]-th packed rows) first, then folds
+// Combine and weighted sum (Fig. 1, last stage). Each wave takes one
+// (token, 1 KiB column slice): every lane loads its 16-byte chunk of the K
+// expert rows (rows pos[t][j] of the packed expert outputs) together, folds
 // them into eight fp32 accumulators with one fused multiply-add per slot in
-// slot order, and stores the round-to-nearest-even bf16 result (plus the
-// fp32 sums when asked).
+// slot order, and stores the round-to-nearest-even bf16 result (and the fp32
+// sums when asked). A wave issues all its loads before its single store, so
+// no load waits behind a store; loads and stores are non-temporal (every
+// byte is touched once).
 #include "internal.hpp"
 
 namespace cobalt {
@@ -21,55 +23,50 @@ template <bool kF32>
 __global__ __launch_bounds__(kCombineWaves * 64) void combine_kernel(
     const u32x4* __restrict__ eo, const int32_t* __restrict__ pos, const float* __restrict__ gates,
     int64_t T, int K, int64_t nch, int64_t TK, u32x4* __restrict__ y, float* __restrict__ y32) {
-    const int64_t t = (int64_t)blockIdx.x * kCombineWaves + (threadIdx.x >> 6);
-    if (t >= T) return;
-    const int lane = threadIdx.x & 63;
-    int64_t row[kMaxK];
+    const int64_t groups = (nch + 63) / 64;
+    const int64_t item = (int64_t)blockIdx.x * kCombineWaves + (threadIdx.x >> 6);
+    if (item >= T * groups) return;
+    const int64_t t = item / groups;
+    const int64_t c = (item - t * groups) * 64 + (threadIdx.x & 63);
+    u32x4 v[kMaxK];
     float g[kMaxK];
     bool ok[kMaxK];
 #pragma unroll
     for (int j = 0; j < kMaxK; ++j) {
         ok[j] = false;
-        row[j] = 0;
         g[j] = 0.f;
         if (j < K) {
             const int p = __builtin_amdgcn_readfirstlane(pos[t * K + j]);
-            ok[j] = p >= 0 && p < TK;
-            row[j] = (int64_t)p * nch;
+            ok[j] = p >= 0 && p < TK && c < nch;
             g[j] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
                                                   __builtin_bit_cast(int, gates[t * K + j])));
+            if (ok[j]) v[j] = __builtin_nontemporal_load(eo + (int64_t)p * nch + c);
         }
     }
-    u32x4* yrow = y + t * nch;
-    for (int64_t c = lane; c < nch; c += 64) {
-        u32x4 v[kMaxK];
+    if (c >= nch) return;
+    float acc[8];
 #pragma unroll
-        for (int j = 0; j < kMaxK; ++j)
-            if (ok[j]) v[j] = __builtin_nontemporal_load(eo + row[j] + c);
-        float acc[8];
+    for (int q = 0; q < 8; ++q) acc[q] = 0.f;
 #pragma unroll
-        for (int q = 0; q < 8; ++q) acc[q] = 0.f;
+    for (int j = 0; j < kMaxK; ++j) {
+        if (!ok[j]) continue;
 #pragma unroll
-        for (int j = 0; j < kMaxK; ++j) {
-            if (!ok[j]) continue;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const float lo = __uint_as_float(v[j][q] << 16);
-                const float hi = __uint_as_float(v[j][q] & 0xffff0000u);
-                acc[2 * q] = __builtin_fmaf(g[j], lo, acc[2 * q]);
-                acc[2 * q + 1] = __builtin_fmaf(g[j], hi, acc[2 * q + 1]);
-            }
+        for (int q = 0; q < 4; ++q) {
+            const float lo = __uint_as_float(v[j][q] << 16);
+            const float hi = __uint_as_float(v[j][q] & 0xffff0000u);
+            acc[2 * q] = __builtin_fmaf(g[j], lo, acc[2 * q]);
+            acc[2 * q + 1] = __builtin_fmaf(g[j], hi, acc[2 * q + 1]);
         }
-        u32x4 out;
+    }
+    u32x4 out;
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            out[q] = f32_to_bf16_rne(acc[2 * q]) | (f32_to_bf16_rne(acc[2 * q + 1]) << 16);
-        __builtin_nontemporal_store(out, yrow + c);
-        if (kF32) {
-            float4* o = (float4*)(y32 + (t * nch + c) * 8);
-            o[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-            o[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
-        }
+    for (int q = 0; q < 4; ++q)
+        out[q] = f32_to_bf16_rne(acc[2 * q]) | (f32_to_bf16_rne(acc[2 * q + 1]) << 16);
+    __builtin_nontemporal_store(out, y + t * nch + c);
+    if (kF32) {
+        float4* o = (float4*)(y32 + (t * nch + c) * 8);
+        o[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        o[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
     }
 }
 
@@ -78,7 +75,8 @@ __global__ __launch_bounds__(kCombineWaves * 64) void combine_kernel(
 cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* gates, int64_t T,
                              int K, int64_t d, void* y, float* y32, hipStream_t s) {
     const int64_t nch = d / 8;
-    const dim3 grid((unsigned)((T + kCombineWaves - 1) / kCombineWaves));
+    const int64_t items = T * ((nch + 63) / 64);
+    const dim3 grid((unsigned)((items + kCombineWaves - 1) / kCombineWaves));
     if (y32)
         hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(kCombineWaves * 64), 0, s,
                            (const u32x4*)eo, pos, gates, T, K, nch, T * K, (u32x4*)y, y32);

@@ -15,11 +15,12 @@
 //   count  send_counts[s][r] (LDS window over the block's sources, global
 //          atomics to flush)
 //   scan   one workgroup: send_offsets and base[s][r] = offsets - colprefix
+//          (counts staged in LDS when G <= 128)
 //   rank   per tile: wave multi-split ranks (ballots over the bits of r),
 //          per-wave running counts in LDS, aggregates published, look-back
 //          over predecessor tiles per destination, then pos
-//   copy   each wave reads one token row of x once into registers and
-//          stores it to its K packed rows with 16-byte non-temporal stores
+//   copy   each wave reads a 1-2 KiB slice of one token row of x once
+//          into registers and stores it to the token's K packed rows
 #include <algorithm>
 
 #include "internal.hpp"
@@ -31,6 +32,7 @@ constexpr int kInitThreads = 256;
 constexpr int kCountThreads = 256;
 constexpr int kCountWin = 8192;  // LDS bins: (source - first source) * G + destination
 constexpr int kScanThreads = 1024;
+constexpr int kScanLds = 16384;  // G*G entries staged in LDS (G <= 128)
 constexpr int kRankWaves = 4;
 constexpr int kRankChunks = 8;
 constexpr int kRankThreads = kRankWaves * 64;
@@ -132,19 +134,30 @@ __device__ int64_t block_exclusive_scan(int64_t v, int64_t* total) {
     return before;
 }
 
+// With G*G <= kScanLds the counts and offsets are staged in LDS, so the
+// sequential column pass reads LDS instead of global memory.
+template <bool kLds>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __restrict__ counts,
                                                             int G, int64_t* __restrict__ offsets,
                                                             int32_t* __restrict__ base) {
+    __shared__ int32_t c_lds[kLds ? kScanLds : 1];
+    __shared__ int32_t o_lds[kLds ? kScanLds : 1];
     const int64_t n = (int64_t)G * G;
+    if (kLds) {
+        for (int64_t b = threadIdx.x; b < n; b += kScanThreads) c_lds[b] = counts[b];
+        __syncthreads();
+    }
+    auto cnt = [&](int64_t b) -> int64_t { return kLds ? c_lds[b] : counts[b]; };
     const int64_t seg = (n + kScanThreads - 1) / kScanThreads;
     const int64_t lo = min(n, (int64_t)threadIdx.x * seg), hi = min(n, lo + seg);
     int64_t local = 0;
-    for (int64_t b = lo; b < hi; ++b) local += counts[b];
+    for (int64_t b = lo; b < hi; ++b) local += cnt(b);
     int64_t total = 0;
     int64_t run = block_exclusive_scan(local, &total);
     for (int64_t b = lo; b < hi; ++b) {
         offsets[b] = run;
-        run += counts[b];
+        if (kLds) o_lds[b] = (int32_t)run;
+        run += cnt(b);
     }
     if (threadIdx.x == 0) offsets[n] = total;
     __syncthreads();
@@ -152,8 +165,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __res
         int64_t col = 0;
         for (int s = 0; s < G; ++s) {
             const int64_t b = (int64_t)s * G + r;
-            base[b] = (int32_t)(offsets[b] - col);
-            col += counts[b];
+            base[b] = (int32_t)((kLds ? (int64_t)o_lds[b] : offsets[b]) - col);
+            col += cnt(b);
         }
     }
 }
@@ -261,66 +274,33 @@ __global__ __launch_bounds__(kRankThreads) void rank_kernel(
     }
 }
 
-// Row copy. CPL = 16-byte chunks per lane (row of nch chunks, nch <= 64*CPL).
-template <int CPL>
+// Row copy. Each wave takes one (token, column group): it loads CG 16-byte
+// chunks per lane of x[t] (64*CG chunks, a contiguous 1-2 KiB slice of the
+// row) once, then stores them to the K packed rows of the token. Small
+// per-wave state keeps many waves in flight; plain stores sustain a higher
+// write rate than non-temporal ones on this access pattern.
+template <int CG>
 __global__ __launch_bounds__(kCopyWaves * 64) void copy_kernel(
     const u32x4* __restrict__ x, const int32_t* __restrict__ pos, int64_t T, int K, int64_t nch,
     int64_t TK, u32x4* __restrict__ packed) {
-    const int64_t t = (int64_t)blockIdx.x * kCopyWaves + (threadIdx.x >> 6);
-    if (t >= T) return;
-    const int lane = threadIdx.x & 63;
+    const int64_t groups = (nch + 64 * CG - 1) / (64 * CG);
+    const int64_t item = (int64_t)blockIdx.x * kCopyWaves + (threadIdx.x >> 6);
+    if (item >= T * groups) return;
+    const int64_t t = item / groups;
+    const int64_t c0 = (item - t * groups) * 64 * CG + (threadIdx.x & 63);
     const u32x4* row = x + t * nch;
-    u32x4 v[CPL];
+    u32x4 v[CG];
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-        const int64_t c = lane + 64 * i;
-        if (c < nch) v[i] = __builtin_nontemporal_load(row + c);
-    }
+    for (int i = 0; i < CG; ++i)
+        if (c0 + 64 * i < nch) v[i] = __builtin_nontemporal_load(row + c0 + 64 * i);
     for (int j = 0; j < K; ++j) {
         const int p = __builtin_amdgcn_readfirstlane(pos[t * K + j]);
         if (p < 0 || p >= TK) continue;
         u32x4* dst = packed + (int64_t)p * nch;
 #pragma unroll
-        for (int i = 0; i < CPL; ++i) {
-            const int64_t c = lane + 64 * i;
-            if (c < nch) __builtin_nontemporal_store(v[i], dst + c);
-        }
+        for (int i = 0; i < CG; ++i)
+            if (c0 + 64 * i < nch) dst[c0 + 64 * i] = v[i];
     }
-}
-
-// Rows longer than 64*16 chunks: the same copy, 16 chunks per lane at a time.
-__global__ __launch_bounds__(kCopyWaves * 64) void copy_kernel_long(
-    const u32x4* __restrict__ x, const int32_t* __restrict__ pos, int64_t T, int K, int64_t nch,
-    int64_t TK, u32x4* __restrict__ packed) {
-    const int64_t t = (int64_t)blockIdx.x * kCopyWaves + (threadIdx.x >> 6);
-    if (t >= T) return;
-    const int lane = threadIdx.x & 63;
-    const u32x4* row = x + t * nch;
-    for (int64_t c0 = 0; c0 < nch; c0 += 64 * 16) {
-        u32x4 v[16];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int64_t c = c0 + lane + 64 * i;
-            if (c < nch) v[i] = __builtin_nontemporal_load(row + c);
-        }
-        for (int j = 0; j < K; ++j) {
-            const int p = __builtin_amdgcn_readfirstlane(pos[t * K + j]);
-            if (p < 0 || p >= TK) continue;
-            u32x4* dst = packed + (int64_t)p * nch;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int64_t c = c0 + lane + 64 * i;
-                if (c < nch) __builtin_nontemporal_store(v[i], dst + c);
-            }
-        }
-    }
-}
-
-template <int CPL>
-void launch_copy_cpl(dim3 grid, hipStream_t s, const u32x4* x, const int32_t* pos, int64_t T,
-                     int K, int64_t nch, int64_t TK, u32x4* packed) {
-    hipLaunchKernelGGL(copy_kernel<CPL>, grid, dim3(kCopyWaves * 64), 0, s, x, pos, T, K, nch, TK,
-                       packed);
 }
 
 }  // namespace
@@ -356,8 +336,12 @@ cobalt_status launch_dispatch(const int32_t* assigned, const int32_t* src, int64
                            T, K, G, tok_per_src, tok_per_blk, counts);
         COBALT_LAUNCH_CHECK();
     }
-    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(kScanThreads), 0, s, counts, G, offsets,
-                       w.base);
+    if ((int64_t)G * G <= kScanLds)
+        hipLaunchKernelGGL(scan_kernel<true>, dim3(1), dim3(kScanThreads), 0, s, counts, G,
+                           offsets, w.base);
+    else
+        hipLaunchKernelGGL(scan_kernel<false>, dim3(1), dim3(kScanThreads), 0, s, counts, G,
+                           offsets, w.base);
     COBALT_LAUNCH_CHECK();
     if (T == 0) return COBALT_OK;
     hipLaunchKernelGGL(rank_kernel, dim3((unsigned)w.ntiles), dim3(kRankThreads), 0, s, assigned,
@@ -366,33 +350,16 @@ cobalt_status launch_dispatch(const int32_t* assigned, const int32_t* src, int64
     if (!x) return COBALT_OK;
 
     const int64_t nch = d / 8;
-    const dim3 grid((unsigned)((T + kCopyWaves - 1) / kCopyWaves));
     const u32x4* xv = (const u32x4*)x;
     u32x4* pv = (u32x4*)packed;
-    const int64_t cpl = (nch + 63) / 64;
-    switch (cpl) {
-#define COBALT_COPY_CASE(n) \
-    case n: launch_copy_cpl<n>(grid, s, xv, pos, T, K, nch, TK, pv); break;
-        COBALT_COPY_CASE(1)
-        COBALT_COPY_CASE(2)
-        COBALT_COPY_CASE(3)
-        COBALT_COPY_CASE(4)
-        COBALT_COPY_CASE(5)
-        COBALT_COPY_CASE(6)
-        COBALT_COPY_CASE(7)
-        COBALT_COPY_CASE(8)
-        COBALT_COPY_CASE(9)
-        COBALT_COPY_CASE(10)
-        COBALT_COPY_CASE(11)
-        COBALT_COPY_CASE(12)
-        COBALT_COPY_CASE(13)
-        COBALT_COPY_CASE(14)
-        COBALT_COPY_CASE(15)
-        COBALT_COPY_CASE(16)
-#undef COBALT_COPY_CASE
-        default:
-            hipLaunchKernelGGL(copy_kernel_long, grid, dim3(kCopyWaves * 64), 0, s, xv, pos, T, K,
-                               nch, TK, pv);
+    if (nch >= 128) {
+        const int64_t items = T * ((nch + 127) / 128);
+        hipLaunchKernelGGL(copy_kernel<2>, dim3((unsigned)((items + kCopyWaves - 1) / kCopyWaves)),
+                           dim3(kCopyWaves * 64), 0, s, xv, pos, T, K, nch, TK, pv);
+    } else {
+        const int64_t items = T * ((nch + 63) / 64);
+        hipLaunchKernelGGL(copy_kernel<1>, dim3((unsigned)((items + kCopyWaves - 1) / kCopyWaves)),
+                           dim3(kCopyWaves * 64), 0, s, xv, pos, T, K, nch, TK, pv);
     }
     COBALT_LAUNCH_CHECK();
     return COBALT_OK;

@@ -22,11 +22,9 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 struct DeviceLayout {
     int device;
     int32_t N, g, G, E, S;
-    int32_t ncand;             // 2^(N-1) candidate covers
     uint32_t* node_mask;       // [E]
     uint32_t* rank_mask;       // [E][N]
     int32_t* owner;            // [E]
-    uint16_t* cand;            // [ncand] remote-node masks by (popcount, value)
 };
 
 #define COBALT_LAUNCH_CHECK()                                        \
@@ -42,8 +40,9 @@ struct DeviceInfo {
 cobalt_status device_info(DeviceInfo* out);
 
 // Launchers (argument checks are done by the C entry points).
+size_t coact_workspace_bytes(int64_t T, int E, int lds_bytes);
 cobalt_status launch_coact_stats(const int32_t* topk, int64_t T, int K, int E, uint32_t* coact,
-                                 uint32_t* count, hipStream_t s);
+                                 uint32_t* count, void* ws, size_t ws_bytes, hipStream_t s);
 cobalt_status launch_assign(const DeviceLayout& L, const int32_t* topk, const int32_t* src,
                             int64_t T, int K, uint64_t key, int mode, int32_t* out,
                             uint16_t* remote, hipStream_t s);

@@ -52,6 +52,7 @@ class RoutingStep:
             raise ValueError(expert_out)
         self.y = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
         self.workspace = B.workspace_for(T, K, G, device=dev)
+        self.stats_workspace = B.stats_workspace_for(T, K, E, device=dev)
 
     def set_routing(self, step: int, route_device=None):
         rd = self.device if route_device is None else route_device
@@ -68,7 +69,8 @@ class RoutingStep:
 
     # the four calls of one step ------------------------------------------
     def stats(self, stream=None):
-        B.cobalt_coact_stats(self.topk, self.w.E, self.coact, self.count, stream=stream)
+        B.cobalt_coact_stats(self.topk, self.w.E, self.coact, self.count, self.stats_workspace,
+                             stream=stream)
 
     def assign(self, mode=0, stream=None):
         B.cobalt_assign(self.layout, self.topk, self.src, self.seed, self.step, mode,

@@ -47,6 +47,11 @@ def test_status_strings():
 
 def test_workspace_size_query():
     L = B.lib()
+    s3 = L.cobalt_coact_stats_workspace_bytes(131072, 8, 256)
+    # one 32-bit partial histogram of the pair triangle per 2048-token chunk
+    assert s3 >= 64 * 256 * 255 // 2 * 4 and s3 % 256 == 0
+    assert L.cobalt_coact_stats_workspace_bytes(100, 2, 4096) > 0
+    assert L.cobalt_coact_stats_workspace_bytes(100, 2, 4097) == 0
     a = L.cobalt_dispatch_workspace_bytes(131072, 8, 64)
     b = L.cobalt_dispatch_workspace_bytes(4096, 2, 8)
     assert a > b > 0 and a % 256 == 0
@@ -63,10 +68,15 @@ def test_argument_checks_reject_before_device_work():
     L = B.lib()
     fake = _p(4096)  # never dereferenced: every call below fails its host checks
     # coact_stats: null output, K out of range, E out of range
-    assert L.cobalt_coact_stats(fake, 10, 2, 16, None, None, None) == EINVAL
-    assert L.cobalt_coact_stats(fake, 10, 17, 16, fake, None, None) == EINVAL
-    assert L.cobalt_coact_stats(fake, 10, 2, 0, fake, None, None) == EINVAL
-    assert L.cobalt_coact_stats(fake, 1 << 28, 8, 16, fake, None, None) == EUNSUPPORTED
+    big = 1 << 40
+    assert L.cobalt_coact_stats(fake, 10, 2, 16, None, None, fake, big, None) == EINVAL
+    assert L.cobalt_coact_stats(fake, 10, 17, 16, fake, None, fake, big, None) == EINVAL
+    assert L.cobalt_coact_stats(fake, 10, 2, 0, fake, None, fake, big, None) == EINVAL
+    assert L.cobalt_coact_stats(fake, 10, 2, 16, fake, None, None, big, None) == EINVAL
+    assert L.cobalt_coact_stats(fake, 10, 2, 16, fake, None, _p(4100), big, None) == EINVAL
+    assert L.cobalt_coact_stats(fake, 10, 2, 16, fake, None, fake, 16, None) == EINVAL
+    assert L.cobalt_coact_stats(fake, 1 << 28, 8, 16, fake, None, fake, big,
+                                None) == EUNSUPPORTED
     # assign: null layout, bad mode
     assert L.cobalt_assign(None, fake, None, 8, 2, 0, 0, 0, fake, None, None) == EINVAL
     assert L.cobalt_assign(fake, fake, None, 8, 2, 0, 0, 7, fake, None, None) == EINVAL

@@ -45,7 +45,7 @@ def run_path(w, seed, topk, gates, table, owner, src=None, x_bits=None, eo_bits=
     t_src = None if src is None else dev_i32(src)
     coact = torch.zeros(E, E, dtype=torch.int32, device="cuda")
     count = torch.zeros(E, dtype=torch.int32, device="cuda")
-    B.cobalt_coact_stats(t_topk, E, coact, count)
+    B.cobalt_coact_stats(t_topk, E, coact, count, B.stats_workspace_for(T, K, E))
     assigned = torch.full((T, K), -7, dtype=torch.int32, device="cuda")
     remote = torch.zeros(T, dtype=torch.int16, device="cuda")
     B.cobalt_assign(L, t_topk, t_src, seed, step, mode, assigned, remote)
@@ -157,22 +157,27 @@ def test_statistics_accumulate_across_calls():
     cnt = np.zeros(E, np.uint32)
     for step in range(3):
         topk, _ = W.routing(w, 4, step=step)
-        B.cobalt_coact_stats(topk.cuda(), E, coact, count)
+        B.cobalt_coact_stats(topk.cuda(), E, coact, count, B.stats_workspace_for(w.T, w.K, E))
         C, cnt = oracle.coact_stats(topk.numpy(), E, C, cnt)
     torch.cuda.synchronize()
     assert np.array_equal(u32(coact), C) and np.array_equal(u32(count), cnt)
 
 
-@pytest.mark.parametrize("E", [384, 1024, 2])
-def test_statistics_row_bands(E):
-    """E = 384 and 1024 need several LDS row bands of the pair triangle."""
-    rng = np.random.default_rng(E)
-    T, K = 3000, 8 if E > 8 else 2
-    topk = np.stack([rng.choice(E, size=K, replace=False) for _ in range(T)]).astype(np.int32)
+@pytest.mark.parametrize("E,T", [(384, 3000), (384, 70001), (1024, 3000), (4096, 2500),
+                                 (2, 3000), (1, 100), (256, 131072 + 77)])
+def test_statistics_layouts(E, T):
+    """Pair histograms kept in LDS as 32-bit bins (E = 256), two 16-bit bins
+    per word (E = 384) and row bands (E = 1024, 4096), over one or many
+    token chunks with ragged tails."""
+    rng = np.random.default_rng(E + T)
+    K = min(8, E)
+    topk = np.argsort(rng.random((T, E)), axis=1)[:, :K].astype(np.int32)
     coact = torch.zeros(E, E, dtype=torch.int32, device="cuda")
-    B.cobalt_coact_stats(dev_i32(topk), E, coact, None)
-    C, _ = oracle.coact_stats(topk, E)
+    count = torch.zeros(E, dtype=torch.int32, device="cuda")
+    B.cobalt_coact_stats(dev_i32(topk), E, coact, count, B.stats_workspace_for(T, K, E))
+    C, cnt = oracle.coact_stats(topk, E)
     assert np.array_equal(u32(coact), C)
+    assert np.array_equal(u32(count), cnt)
 
 
 def _custom(N, g, E, S, K, T, d, seed, extra_per_rank=None):
@@ -214,7 +219,7 @@ def test_empty_inputs_are_no_ops():
     L = B.cobalt_layout_create(w.N, w.g, w.E, w.S, table, owner)
     e0 = torch.zeros(0, w.K, dtype=torch.int32, device="cuda")
     coact = torch.zeros(w.E, w.E, dtype=torch.int32, device="cuda")
-    B.cobalt_coact_stats(e0, w.E, coact)
+    B.cobalt_coact_stats(e0, w.E, coact, None, B.stats_workspace_for(0, w.K, w.E))
     B.cobalt_assign(L, e0, None, 0, 0, 0, e0.clone())
     counts = torch.full((w.G, w.G), 5, dtype=torch.int32, device="cuda")
     offsets = torch.full((w.G * w.G + 1,), 5, dtype=torch.int64, device="cuda")
