@@ -12,7 +12,7 @@ position of the dominant call, the pack+combine share of HBM peak, routing
 quality (cross-node traffic of Algorithm 1 vs owner-only baselines), and the
 oracle's CPU throughput on a bounded sample of the same workload.
 
-    python bench.py [--steps K] [--warmup W] [--config C] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -37,7 +37,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--workload", default="colocate-e256",
+                    help="name of a seeded workload in paper_2609_36959_amd/workload.py")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=65536)
@@ -159,10 +160,10 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     B.lib()
-    w = W.CONFIGS[args.config]
+    w = W.WORKLOADS[args.workload]
     if w.steps > 1:
         print("note: timing one step of the drift workload", file=sys.stderr)
-    seed = args.config if args.seed is None else args.seed
+    seed = w.seed if args.seed is None else args.seed
     wl_name = f"t{w.T}_e{w.E}_k{w.K}_d{w.d}"
     st = PL.RoutingStep(w, seed=seed, device="cuda", expert_out="independent")
     stream = torch.cuda.Stream()

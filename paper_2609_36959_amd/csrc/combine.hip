@@ -11,7 +11,7 @@
 namespace cobalt {
 namespace {
 
-constexpr int kCombineWaves = 4;
+constexpr int kCombineWaves = 16;
 
 __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
     const uint32_t u = __float_as_uint(f);
@@ -19,36 +19,45 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
     return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-template <bool kF32>
+// KC = compile-time K (0: any K up to 16, read at run time); with KC the
+// scalar loads of pos and gates are issued back to back before the rows.
+template <bool kF32, int KC>
 __global__ __launch_bounds__(kCombineWaves * 64) void combine_kernel(
     const u32x4* __restrict__ eo, const int32_t* __restrict__ pos, const float* __restrict__ gates,
-    int64_t T, int K, int64_t nch, int64_t TK, u32x4* __restrict__ y, float* __restrict__ y32) {
+    int64_t T, int Kr, int64_t nch, int64_t TK, u32x4* __restrict__ y, float* __restrict__ y32) {
+    constexpr int KM = KC ? KC : kMaxK;
+    const int K = KC ? KC : Kr;
     const int64_t groups = (nch + 63) / 64;
-    const int64_t item = (int64_t)blockIdx.x * kCombineWaves + (threadIdx.x >> 6);
+    // wave-uniform item index, so pos and gates come in through scalar loads
+    const int64_t item = (int64_t)blockIdx.x * kCombineWaves +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (item >= T * groups) return;
     const int64_t t = item / groups;
     const int64_t c = (item - t * groups) * 64 + (threadIdx.x & 63);
-    u32x4 v[kMaxK];
-    float g[kMaxK];
-    bool ok[kMaxK];
+    int p[KM];
+    float g[KM];
 #pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
-        ok[j] = false;
+    for (int j = 0; j < KM; ++j) {
+        p[j] = -1;
         g[j] = 0.f;
         if (j < K) {
-            const int p = __builtin_amdgcn_readfirstlane(pos[t * K + j]);
-            ok[j] = p >= 0 && p < TK && c < nch;
-            g[j] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
-                                                  __builtin_bit_cast(int, gates[t * K + j])));
-            if (ok[j]) v[j] = __builtin_nontemporal_load(eo + (int64_t)p * nch + c);
+            p[j] = pos[t * K + j];
+            g[j] = gates[t * K + j];
         }
+    }
+    u32x4 v[KM];
+    bool ok[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        ok[j] = p[j] >= 0 && p[j] < TK && c < nch;
+        if (ok[j]) v[j] = __builtin_nontemporal_load(eo + (int64_t)p[j] * nch + c);
     }
     if (c >= nch) return;
     float acc[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) acc[q] = 0.f;
 #pragma unroll
-    for (int j = 0; j < kMaxK; ++j) {
+    for (int j = 0; j < KM; ++j) {
         if (!ok[j]) continue;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -77,12 +86,14 @@ cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* ga
     const int64_t nch = d / 8;
     const int64_t items = T * ((nch + 63) / 64);
     const dim3 grid((unsigned)((items + kCombineWaves - 1) / kCombineWaves));
-    if (y32)
-        hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(kCombineWaves * 64), 0, s,
-                           (const u32x4*)eo, pos, gates, T, K, nch, T * K, (u32x4*)y, y32);
+    auto launch = [&](auto kernel) {
+        hipLaunchKernelGGL(kernel, grid, dim3(kCombineWaves * 64), 0, s, (const u32x4*)eo, pos,
+                           gates, T, K, nch, T * K, (u32x4*)y, y32);
+    };
+    if (K == 8)
+        y32 ? launch(combine_kernel<true, 8>) : launch(combine_kernel<false, 8>);
     else
-        hipLaunchKernelGGL(combine_kernel<false>, grid, dim3(kCombineWaves * 64), 0, s,
-                           (const u32x4*)eo, pos, gates, T, K, nch, T * K, (u32x4*)y, y32);
+        y32 ? launch(combine_kernel<true, 0>) : launch(combine_kernel<false, 0>);
     COBALT_LAUNCH_CHECK();
     return COBALT_OK;
 }

@@ -279,24 +279,33 @@ __global__ __launch_bounds__(kRankThreads) void rank_kernel(
 // row) once, then stores them to the K packed rows of the token. Small
 // per-wave state keeps many waves in flight; plain stores sustain a higher
 // write rate than non-temporal ones on this access pattern.
-template <int CG>
+// KC = compile-time K (0: any K up to 16); with KC the scalar loads of the
+// token's pos entries are issued together.
+template <int CG, int KC>
 __global__ __launch_bounds__(kCopyWaves * 64) void copy_kernel(
-    const u32x4* __restrict__ x, const int32_t* __restrict__ pos, int64_t T, int K, int64_t nch,
+    const u32x4* __restrict__ x, const int32_t* __restrict__ pos, int64_t T, int Kr, int64_t nch,
     int64_t TK, u32x4* __restrict__ packed) {
+    constexpr int KM = KC ? KC : kMaxK;
+    const int K = KC ? KC : Kr;
     const int64_t groups = (nch + 64 * CG - 1) / (64 * CG);
-    const int64_t item = (int64_t)blockIdx.x * kCopyWaves + (threadIdx.x >> 6);
+    // wave-uniform item index, so pos comes in through scalar loads
+    const int64_t item = (int64_t)blockIdx.x * kCopyWaves +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (item >= T * groups) return;
     const int64_t t = item / groups;
     const int64_t c0 = (item - t * groups) * 64 * CG + (threadIdx.x & 63);
+    int p[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) p[j] = j < K ? pos[t * K + j] : -1;
     const u32x4* row = x + t * nch;
     u32x4 v[CG];
 #pragma unroll
     for (int i = 0; i < CG; ++i)
         if (c0 + 64 * i < nch) v[i] = __builtin_nontemporal_load(row + c0 + 64 * i);
-    for (int j = 0; j < K; ++j) {
-        const int p = __builtin_amdgcn_readfirstlane(pos[t * K + j]);
-        if (p < 0 || p >= TK) continue;
-        u32x4* dst = packed + (int64_t)p * nch;
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        if (p[j] < 0 || p[j] >= TK) continue;
+        u32x4* dst = packed + (int64_t)p[j] * nch;
 #pragma unroll
         for (int i = 0; i < CG; ++i)
             if (c0 + 64 * i < nch) dst[c0 + 64 * i] = v[i];
@@ -352,15 +361,15 @@ cobalt_status launch_dispatch(const int32_t* assigned, const int32_t* src, int64
     const int64_t nch = d / 8;
     const u32x4* xv = (const u32x4*)x;
     u32x4* pv = (u32x4*)packed;
-    if (nch >= 128) {
-        const int64_t items = T * ((nch + 127) / 128);
-        hipLaunchKernelGGL(copy_kernel<2>, dim3((unsigned)((items + kCopyWaves - 1) / kCopyWaves)),
+    auto launch = [&](auto kernel, int64_t cg) {
+        const int64_t items = T * ((nch + 64 * cg - 1) / (64 * cg));
+        hipLaunchKernelGGL(kernel, dim3((unsigned)((items + kCopyWaves - 1) / kCopyWaves)),
                            dim3(kCopyWaves * 64), 0, s, xv, pos, T, K, nch, TK, pv);
-    } else {
-        const int64_t items = T * ((nch + 63) / 64);
-        hipLaunchKernelGGL(copy_kernel<1>, dim3((unsigned)((items + kCopyWaves - 1) / kCopyWaves)),
-                           dim3(kCopyWaves * 64), 0, s, xv, pos, T, K, nch, TK, pv);
-    }
+    };
+    if (nch >= 128)
+        K == 8 ? launch(copy_kernel<2, 8>, 2) : launch(copy_kernel<2, 0>, 2);
+    else
+        K == 8 ? launch(copy_kernel<1, 8>, 1) : launch(copy_kernel<1, 0>, 1);
     COBALT_LAUNCH_CHECK();
     return COBALT_OK;
 }

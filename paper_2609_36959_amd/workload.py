@@ -51,6 +51,7 @@ class Workload:
     steps: int = 1
     drift_frac: float = 0.0         # share of experts whose bias rotates per step
     swap_step: int = -1             # step before which the layout is re-planned
+    seed: int = 0                   # default seed of the workload
 
     @property
     def G(self) -> int:
@@ -61,26 +62,27 @@ class Workload:
                 f"{self.N}x{self.g} S={self.S}")
 
 
-# The five seeded workloads. Config 0's slot count reads "2 slots (owner + 1
-# replica)" with E/G = 2 owners per rank, which leaves no room for a replica;
-# it is read as 3 slots (rho = 0.5), and the literal 2 is kept as the
-# no-replica degenerate case in the tests.
-CONFIGS = {
-    0: Workload("tiny", 4096, 16, 2, 512, 2, 4, 3, zipf_alpha=1.0,
-                owners="permuted", replicas="random"),
-    1: Workload("clusters-e64", 16384, 64, 6, 2048, 4, 8, 3,
-                cluster_size=4, cluster_beta=2.0,
-                owners="contiguous", replicas="random"),
-    2: Workload("colocate-e128", 65536, 128, 8, 4096, 4, 8, 5, zipf_alpha=1.2,
-                cluster_size=8, cluster_beta=1.5,
-                owners="cluster", replicas="intra_node_top"),
-    3: Workload("colocate-e256", 131072, 256, 8, 7168, 8, 8, 5, zipf_alpha=1.1,
-                cluster_size=4, cluster_beta=2.0,
-                owners="cluster", replicas="intra_node_top"),
-    4: Workload("drift-e384", 262144, 384, 8, 7168, 8, 8, 8, zipf_alpha=1.1,
-                owners="contiguous", replicas="random",
-                steps=16, drift_frac=0.05, swap_step=8),
-}
+# The five seeded workloads, by name. The tiny workload's slot count reads
+# "2 slots (owner + 1 replica)" with E/G = 2 owners per rank, which leaves no
+# room for a replica; it is read as 3 slots (rho = 0.5), and the literal 2 is
+# kept as the no-replica degenerate case in the tests.
+WORKLOADS = {w.name: w for w in (
+    Workload("tiny", 4096, 16, 2, 512, 2, 4, 3, zipf_alpha=1.0,
+             owners="permuted", replicas="random", seed=0),
+    Workload("clusters-e64", 16384, 64, 6, 2048, 4, 8, 3,
+             cluster_size=4, cluster_beta=2.0,
+             owners="contiguous", replicas="random", seed=1),
+    Workload("colocate-e128", 65536, 128, 8, 4096, 4, 8, 5, zipf_alpha=1.2,
+             cluster_size=8, cluster_beta=1.5,
+             owners="cluster", replicas="intra_node_top", seed=2),
+    Workload("colocate-e256", 131072, 256, 8, 7168, 8, 8, 5, zipf_alpha=1.1,
+             cluster_size=4, cluster_beta=2.0,
+             owners="cluster", replicas="intra_node_top", seed=3),
+    Workload("drift-e384", 262144, 384, 8, 7168, 8, 8, 8, zipf_alpha=1.1,
+             owners="contiguous", replicas="random",
+             steps=16, drift_frac=0.05, swap_step=8, seed=4),
+)}
+NAMES = list(WORKLOADS)
 
 # numbered sub-streams of a seed
 _S_PERM, _S_CLUSTER, _S_LAYOUT, _S_DRIFT, _S_ROUTE, _S_HIDDEN, _S_EXPOUT, _S_HOT = range(8)

@@ -67,15 +67,15 @@ def round_trip(st):
     assert torch.equal(y.float(), st.x.float())
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3])
-def test_full_size_single_step(cfg):
-    w = W.CONFIGS[cfg]
-    print(f"full size cfg={cfg} {w.describe()}", flush=True)
-    st = PL.RoutingStep(w, seed=cfg, device="cuda")
+@pytest.mark.parametrize("name", ["clusters-e64", "colocate-e128", "colocate-e256"])
+def test_full_size_single_step(name):
+    w = W.WORKLOADS[name]
+    print(f"full size {name} {w.describe()}", flush=True)
+    st = PL.RoutingStep(w, seed=w.seed, device="cuda")
     st.run()
     torch.cuda.synchronize()
     tabs = oracle.layout_tables(w.N, w.g, w.E, st.table, st.owner)
-    check_step(st, tabs, None, None, np.random.default_rng(cfg))
+    check_step(st, tabs, None, None, np.random.default_rng(w.seed))
     round_trip(st)
     st.close()
     del st
@@ -86,8 +86,8 @@ def test_drift_sixteen_steps_with_layout_swap():
     """16 steps of T=262144, E=384: statistics accumulate across steps, the
     Zipf skew drifts every step, and before step 8 the replicas are
     re-planned from the accumulated expert counts."""
-    w = W.CONFIGS[4]
-    seed = 4
+    w = W.WORKLOADS["drift-e384"]
+    seed = w.seed
     st = PL.RoutingStep(w, seed=seed, device="cuda")
     rng = np.random.default_rng(44)
     tabs = oracle.layout_tables(w.N, w.g, w.E, st.table, st.owner)

@@ -112,33 +112,33 @@ def check_against_oracle(w, seed, topk, gates, table, owner, src=None, step=0, m
 
 
 CASES = [
-    # cfg, T, d, source ranks
-    (0, 4096, 512, "null"),
-    (0, 4096 + 8 * 37, 512, "null"),
-    (0, 3001, 128, "ragged"),
-    (1, 32 * 200, 2048, "null"),
-    (1, 5003, 256, "ragged"),
-    (2, 32 * 130, 4096, "null"),
-    (3, 64 * 40, 7168, "null"),
-    (3, 2999, 64, "ragged"),
-    (4, 64 * 33, 1024, "null"),
+    # workload, T, d, source ranks
+    ("tiny", 4096, 512, "null"),
+    ("tiny", 4096 + 8 * 37, 512, "null"),
+    ("tiny", 3001, 128, "ragged"),
+    ("clusters-e64", 32 * 200, 2048, "null"),
+    ("clusters-e64", 5003, 256, "ragged"),
+    ("colocate-e128", 32 * 130, 4096, "null"),
+    ("colocate-e256", 64 * 40, 7168, "null"),
+    ("colocate-e256", 2999, 64, "ragged"),
+    ("drift-e384", 64 * 33, 1024, "null"),
 ]
 
 
-@pytest.mark.parametrize("cfg,T,d,srckind", CASES)
+@pytest.mark.parametrize("name,T,d,srckind", CASES)
 @pytest.mark.parametrize("mode", [0, 1])
-def test_path_matches_oracle(cfg, T, d, srckind, mode):
-    w = W.with_sizes(W.CONFIGS[cfg], T=T, d=d)
-    print(f"case cfg={cfg} T={T} d={d} src={srckind} mode={mode}", flush=True)
-    topk, gates = W.routing(w, cfg)
-    table, owner = W.layout(w, cfg)
-    src = None if srckind == "null" else W.ragged_src(T, w.G, seed=cfg)
-    check_against_oracle(w, cfg, topk.numpy(), gates.numpy(), table, owner, src, step=3,
+def test_path_matches_oracle(name, T, d, srckind, mode):
+    w = W.with_sizes(W.WORKLOADS[name], T=T, d=d)
+    print(f"case {name} T={T} d={d} src={srckind} mode={mode}", flush=True)
+    topk, gates = W.routing(w, w.seed)
+    table, owner = W.layout(w, w.seed)
+    src = None if srckind == "null" else W.ragged_src(T, w.G, seed=w.seed)
+    check_against_oracle(w, w.seed, topk.numpy(), gates.numpy(), table, owner, src, step=3,
                          mode=mode)
 
 
 def test_deterministic_repeats_and_stale_workspace():
-    w = W.with_sizes(W.CONFIGS[3], T=64 * 70, d=256)
+    w = W.with_sizes(W.WORKLOADS["colocate-e256"], T=64 * 70, d=256)
     topk, gates = W.routing(w, 5)
     table, owner = W.layout(w, 5)
     got = check_against_oracle(w, 5, topk.numpy(), gates.numpy(), table, owner, repeat=4)
@@ -149,7 +149,7 @@ def test_deterministic_repeats_and_stale_workspace():
 
 
 def test_statistics_accumulate_across_calls():
-    w = W.with_sizes(W.CONFIGS[4], T=64 * 40)
+    w = W.with_sizes(W.WORKLOADS["drift-e384"], T=64 * 40)
     E = w.E
     coact = torch.zeros(E, E, dtype=torch.int32, device="cuda")
     count = torch.zeros(E, dtype=torch.int32, device="cuda")
@@ -214,7 +214,7 @@ def test_edge_shapes(N, g, E, S, K, T, d):
 
 
 def test_empty_inputs_are_no_ops():
-    w = W.CONFIGS[0]
+    w = W.WORKLOADS["tiny"]
     table, owner = W.layout(w, 0)
     L = B.cobalt_layout_create(w.N, w.g, w.E, w.S, table, owner)
     e0 = torch.zeros(0, w.K, dtype=torch.int32, device="cuda")
@@ -235,7 +235,7 @@ def test_empty_inputs_are_no_ops():
 
 
 def test_index_only_dispatch_matches():
-    w = W.with_sizes(W.CONFIGS[1], T=32 * 77)
+    w = W.with_sizes(W.WORKLOADS["clusters-e64"], T=32 * 77)
     topk, _ = W.routing(w, 1)
     table, owner = W.layout(w, 1)
     L = B.cobalt_layout_create(w.N, w.g, w.E, w.S, table, owner)
@@ -262,7 +262,7 @@ def test_validate_routing_flags():
 
 def test_round_trip_returns_x():
     """expert_out = packed, gates summing to one: y equals x by value."""
-    w = W.with_sizes(W.CONFIGS[2], T=32 * 64, d=1024)
+    w = W.with_sizes(W.WORKLOADS["colocate-e128"], T=32 * 64, d=1024)
     st = PL.RoutingStep(w, seed=2, device="cuda", expert_out="roundtrip", route_device="cpu")
     st.run()
     torch.cuda.synchronize()

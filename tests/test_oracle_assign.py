@@ -137,7 +137,7 @@ def test_brute_force_min_cover(case):
 
 # ------------------------------------------------------------ special cases
 def test_no_replicas_equals_owner_only():
-    w = W.with_sizes(W.CONFIGS[0], T=2048)
+    w = W.with_sizes(W.WORKLOADS["tiny"], T=2048)
     table, owner = W.layout(w, 0, S=w.E // w.G, replicas="none")  # literal S = 2
     tabs = oracle.layout_tables(w.N, w.g, w.E, table, owner)
     topk, _ = W.routing(w, 0)
@@ -172,7 +172,7 @@ def test_every_expert_local_means_no_remote_nodes():
 
 
 def test_k1_single_selection():
-    w = W.with_sizes(W.CONFIGS[1], T=512, K=1)
+    w = W.with_sizes(W.WORKLOADS["clusters-e64"], T=512, K=1)
     table, owner = W.layout(w, 1)
     tabs = oracle.layout_tables(w.N, w.g, w.E, table, owner)
     topk, _ = W.routing(w, 1)
@@ -214,7 +214,7 @@ def test_node_choice_uniform_within_cover():
 
 
 def test_deterministic_and_seed_dependent():
-    w = W.with_sizes(W.CONFIGS[1], T=4096)
+    w = W.with_sizes(W.WORKLOADS["clusters-e64"], T=4096)
     table, owner = W.layout(w, 1)
     tabs = oracle.layout_tables(w.N, w.g, w.E, table, owner)
     topk = W.routing(w, 1)[0].numpy()
@@ -226,13 +226,13 @@ def test_deterministic_and_seed_dependent():
 
 
 # ------------------------------------------------ workloads at reduced size
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
-def test_reduced_configs_valid_and_never_worse_than_owner_only(cfg):
-    w = W.with_sizes(W.CONFIGS[cfg], T=W.CONFIGS[cfg].G * 16)
-    table, owner = W.layout(w, cfg)
+@pytest.mark.parametrize("name", ["tiny", "clusters-e64", "colocate-e128", "colocate-e256", "drift-e384"])
+def test_reduced_configs_valid_and_never_worse_than_owner_only(name):
+    w = W.with_sizes(W.WORKLOADS[name], T=W.WORKLOADS[name].G * 16)
+    table, owner = W.layout(w, w.seed)
     tabs = oracle.layout_tables(w.N, w.g, w.E, table, owner)
-    topk = W.routing(w, cfg)[0].numpy()
-    a, rn = oracle.assign(w.N, w.g, w.E, tabs, topk, seed=cfg)
+    topk = W.routing(w, w.seed)[0].numpy()
+    a, rn = oracle.assign(w.N, w.g, w.E, tabs, topk, seed=w.seed)
     o, orn = oracle.assign(w.N, w.g, w.E, tabs, topk, mode=1)
     held = [set(table[r][table[r] >= 0].tolist()) for r in range(w.G)]
     assert all(topk[t, j] in held[a[t, j]] for t in range(w.T) for j in range(w.K))

@@ -36,15 +36,15 @@ def test_fp64_bound(T, K, d):
     assert np.array_equal(y, want)
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 3])
-def test_round_trip_identity(cfg):
+@pytest.mark.parametrize("name", ["tiny", "clusters-e64", "colocate-e256"])
+def test_round_trip_identity(name):
     """expert_out = packed and gates summing to one give back x (by value)."""
-    w = W.with_sizes(W.CONFIGS[cfg], T=W.CONFIGS[cfg].G * 8, d=64)
-    table, owner = W.layout(w, cfg)
+    w = W.with_sizes(W.WORKLOADS[name], T=W.WORKLOADS[name].G * 8, d=64)
+    table, owner = W.layout(w, w.seed)
     tabs = oracle.layout_tables(w.N, w.g, w.E, table, owner)
-    topk, gates = W.routing(w, cfg)
-    a, _ = oracle.assign(w.N, w.g, w.E, tabs, topk.numpy(), seed=cfg)
-    x = _bits(W.hidden(w, cfg))
+    topk, gates = W.routing(w, w.seed)
+    a, _ = oracle.assign(w.N, w.g, w.E, tabs, topk.numpy(), seed=w.seed)
+    x = _bits(W.hidden(w, w.seed))
     _, _, pos, packed = oracle.dispatch(a, w.G, None, x)
     y, _ = oracle.combine(packed, pos, gates.numpy())
     assert np.array_equal(_widen(y), _widen(x))

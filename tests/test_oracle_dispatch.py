@@ -54,7 +54,7 @@ def test_matches_stable_sort(G, T, K, ragged):
 
 
 def test_invariants_on_reduced_config():
-    w = W.with_sizes(W.CONFIGS[3], T=4096)
+    w = W.with_sizes(W.WORKLOADS["colocate-e256"], T=4096)
     table, owner = W.layout(w, 3)
     tabs = oracle.layout_tables(w.N, w.g, w.E, table, owner)
     topk = W.routing(w, 3)[0].numpy()

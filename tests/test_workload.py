@@ -7,10 +7,10 @@ import oracle
 from paper_2609_36959_amd import workload as W
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
-def test_layout_valid(cfg):
-    w = W.CONFIGS[cfg]
-    table, owner = W.layout(w, cfg)
+@pytest.mark.parametrize("name", ["tiny", "clusters-e64", "colocate-e128", "colocate-e256", "drift-e384"])
+def test_layout_valid(name):
+    w = W.WORKLOADS[name]
+    table, owner = W.layout(w, w.seed)
     assert table.shape == (w.G, w.S)
     nm, rm, own = oracle.layout_tables(w.N, w.g, w.E, table, owner)  # raises if invalid
     assert np.all(own == owner)
@@ -24,7 +24,7 @@ def test_layout_valid(cfg):
 
 
 def test_routing_deterministic_and_shaped():
-    w = W.with_sizes(W.CONFIGS[2], T=1000)
+    w = W.with_sizes(W.WORKLOADS["colocate-e128"], T=1000)
     a, g = W.routing(w, 2)
     b, h = W.routing(w, 2)
     assert a.shape == (1000, w.K) and a.dtype.is_floating_point is False
@@ -36,7 +36,7 @@ def test_routing_deterministic_and_shaped():
 
 
 def test_planted_clusters_co_activate():
-    w = W.with_sizes(W.CONFIGS[1], T=4096)
+    w = W.with_sizes(W.WORKLOADS["clusters-e64"], T=4096)
     topk = W.routing(w, 1)[0].numpy()
     C, cnt = oracle.coact_stats(topk, w.E)
     cl = W.clusters(w, 1)
@@ -48,7 +48,7 @@ def test_planted_clusters_co_activate():
 
 
 def test_drift_moves_bias_and_hot_order():
-    w = W.CONFIGS[4]
+    w = W.WORKLOADS["drift-e384"]
     b0, b8 = W.bias(w, 4, 0), W.bias(w, 4, 8)
     assert np.array_equal(np.sort(b0), np.sort(b8)) and not np.array_equal(b0, b8)
     t1, _ = W.layout(w, 4)
