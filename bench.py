@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=65536)
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the extra timing of the step replayed as a HIP graph")
     return ap.parse_args()
 
 
@@ -161,8 +163,6 @@ def main():
     torch.cuda.set_device(0)
     B.lib()
     w = W.WORKLOADS[args.workload]
-    if w.steps > 1:
-        print("note: timing one step of the drift workload", file=sys.stderr)
     seed = w.seed if args.seed is None else args.seed
     wl_name = f"t{w.T}_e{w.E}_k{w.K}_d{w.d}"
     st = PL.RoutingStep(w, seed=seed, device="cuda", expert_out="independent")
@@ -186,12 +186,36 @@ def main():
     torch.cuda.synchronize()
     assert int(st.offsets[-1].item()) == w.T * w.K, "dispatch placed the wrong number of rows"
 
+    # A multi-step (drift) workload cycles through its per-step routings:
+    # statistics accumulate over a cycle and the replicas are re-planned
+    # from them before the swap step. The re-plan is host work between
+    # steps, so such runs are timed by the sum of per-step HIP events.
+    drift = w.steps > 1
+    if drift:
+        routes = [W.routing(w, seed, step=s, device="cuda") for s in range(w.steps)]
+        first_layout = (st.table, st.owner)
+        st.coact.zero_()
+        st.count.zero_()
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)]
            for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     with torch.cuda.stream(stream):
         for k in range(args.steps):
+            if drift:
+                s = k % w.steps
+                if s == 0 and k > 0:
+                    st.coact.zero_()
+                    st.count.zero_()
+                    stream.synchronize()
+                    st.set_layout(*first_layout)
+                if s == w.swap_step:
+                    stream.synchronize()
+                    counts = st.count.cpu().numpy().view("uint32").astype("int64")
+                    hot = sorted(range(w.E), key=lambda e: (-counts[e], e))
+                    st.set_layout(*W.layout(w, seed, hot_order=hot, plan=s))
+                st.topk, st.gates = routes[s]
+                st.step = s
             e = evs[k]
             e[0].record(stream)
             for i, f in enumerate(fns):
@@ -199,6 +223,8 @@ def main():
                 e[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    if drift:
+        wall = sum(e[0].elapsed_time(e[-1]) for e in evs) * 1e-3
 
     call_ms = {c: 0.0 for c in calls}
     for e in evs:
@@ -226,7 +252,9 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"co-activation routing step, {w.describe()}, "
-                               f"{w.name}, seed {seed}",
+                               f"{w.name}, seed {seed}" +
+                               (f", {w.steps}-step drift cycle with re-plan before step "
+                                f"{w.swap_step}, timed by per-step events" if drift else ""),
                    "T": w.T, "E": w.E, "K": w.K, "d": w.d, "nodes": w.N,
                    "gpus_per_node": w.g, "slots_per_gpu": w.S,
                    "parallelism": "single GPU; virtual ranks are HBM buffers"},
@@ -238,6 +266,23 @@ def main():
         "call_ms": call_ms,
         "call_gbps": {c: ab[c] / (call_ms[c] * 1e-3) / 1e9 for c in calls},
     }
+    if not drift and not args.no_graph:
+        # the same four calls captured once as a HIP graph and replayed
+        g = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            st.run()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        tg = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        wg = time.perf_counter() - tg
+        result["graph_replay"] = {"value": w.T * args.steps / wg, "unit": "tokens/s",
+                                  "ms_per_step": wg * 1e3 / args.steps}
+        del g
     result["routing"] = routing_quality(st, torch, B, W)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(st, args.cpu_sample_tokens, torch, W, PL)

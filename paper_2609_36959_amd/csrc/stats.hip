@@ -27,6 +27,9 @@
 #include <algorithm>
 #include <climits>
 #include <cmath>
+#include <mutex>
+#include <set>
+#include <utility>
 
 #include "internal.hpp"
 
@@ -272,20 +275,32 @@ cobalt_status launch_coact_stats(const int32_t* topk, int64_t T, int K, int E, u
     uint32_t* part = (uint32_t*)ws;
     uint32_t* cpart = (uint32_t*)((char*)ws + p.part_bytes);
     const dim3 grid((unsigned)(p.nchunks * p.nbands));
-    auto launch = [&](auto kernel) -> cobalt_status {
-        if (p.lds_bytes > 64 * 1024 &&
-            hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)p.lds_bytes) != hipSuccess)
-            return COBALT_EHIP;
+    // The LDS limit of each kernel variant is raised to the device maximum
+    // once per device (host-side only, so the calls stay capturable).
+    auto launch = [&](auto kernel, int variant) -> cobalt_status {
+        static std::mutex mu;
+        static std::set<std::pair<int, int>> raised;
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess) return COBALT_EHIP;
+        {
+            std::lock_guard<std::mutex> lock(mu);
+            if (!raised.count({variant, dev})) {
+                if (hipFuncSetAttribute((const void*)kernel,
+                                        hipFuncAttributeMaxDynamicSharedMemorySize,
+                                        di.lds_bytes) != hipSuccess)
+                    return COBALT_EHIP;
+                raised.insert({variant, dev});
+            }
+        }
         hipLaunchKernelGGL(kernel, grid, dim3(kCountThreads), p.lds_bytes, s, topk, T, K, E,
                            bands, p.nchunks, p.tok_per_chunk, p.band_stride, part, cpart);
         return COBALT_OK;
     };
     cobalt_status st;
     if (K == 8)
-        st = p.half ? launch(coact_count_kernel<true, 8>) : launch(coact_count_kernel<false, 8>);
+        st = p.half ? launch(coact_count_kernel<true, 8>, 0) : launch(coact_count_kernel<false, 8>, 1);
     else
-        st = p.half ? launch(coact_count_kernel<true, 0>) : launch(coact_count_kernel<false, 0>);
+        st = p.half ? launch(coact_count_kernel<true, 0>, 2) : launch(coact_count_kernel<false, 0>, 3);
     if (st != COBALT_OK) return st;
     COBALT_LAUNCH_CHECK();
     const int64_t items = (p.words + (count ? E : 0)) * kReduceLanes;
