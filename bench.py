@@ -112,6 +112,34 @@ def routing_quality(st, torch, B, W):
     return out
 
 
+def stage2_demo(st, torch, B, W):
+    """Per-step intra-node rebalancing (Section 3.2, Stage 2) on this step:
+    the per-replica loads w_er measured on the GPU drive the host greedy
+    re-placement; the step is then re-assigned on the new layout. Reports
+    the rank-load imbalance (max / mean) before and after."""
+    import numpy as np
+    w = st.w
+    st.replica_load.zero_()
+    st.assign()
+    st.load()
+    torch.cuda.synchronize()
+    rl = st.replica_load.cpu().numpy().view(np.uint32).astype(np.float32)
+    before = rl.sum(0)
+    t0 = time.perf_counter()
+    table, owner, pred = B.cobalt_intra_node_rebalance(w.N, w.g, w.E, st.table.shape[1],
+                                                       st.table, st.owner, rl)
+    host_ms = (time.perf_counter() - t0) * 1e3
+    L = B.cobalt_layout_create(w.N, w.g, w.E, table.shape[1], table, owner)
+    a = torch.empty_like(st.assigned)
+    B.cobalt_assign(L, st.topk, st.src, st.seed, st.step, 0, a)
+    after = torch.bincount(a.flatten().long(), minlength=w.G).float().cpu().numpy()
+    B.cobalt_layout_destroy(L)
+    mean = w.T * w.K / w.G
+    return {"imbalance_before": float(before.max() / mean),
+            "imbalance_predicted": float(pred.max() / mean),
+            "imbalance_after": float(after.max() / mean), "host_ms": host_ms}
+
+
 def cpu_baseline(st, n_tokens, torch, W, PL):
     """The oracle, as it stands, on the first n_tokens of the same workload,
     in chunks of 4096 tokens (each chunk a full pass: stats, assign, dispatch
@@ -283,7 +311,18 @@ def main():
         result["graph_replay"] = {"value": w.T * args.steps / wg, "unit": "tokens/s",
                                   "ms_per_step": wg * 1e3 / args.steps}
         del g
+    # calls outside the step: per-replica load counts (the Stage-2 input)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    with torch.cuda.stream(stream):
+        st.load(stream=stream)
+        ev[0].record(stream)
+        for _ in range(args.steps):
+            st.load(stream=stream)
+        ev[1].record(stream)
+    torch.cuda.synchronize()
+    result["extra_calls_ms"] = {"cobalt_replica_load": ev[0].elapsed_time(ev[1]) / args.steps}
     result["routing"] = routing_quality(st, torch, B, W)
+    result["routing"]["stage2_rebalance"] = stage2_demo(st, torch, B, W)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(st, args.cpu_sample_tokens, torch, W, PL)
     st.close()

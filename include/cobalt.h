@@ -175,6 +175,53 @@ cobalt_status cobalt_combine(const void* expert_out, const int32_t* pos, const f
                              void* y, float* y_f32, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Per-replica workload (Section 3.1 workload model: w_er counts the tasks of
+ * expert e executed on rank r; Section 3.2, Stage 2 tracks it per replica).
+ *
+ * topk_idx [T][K] int32 in, assigned_rank [T][K] int32 in (the output of
+ * cobalt_assign), load [E][G] uint32 in/out:
+ *   load[e][r] += #{(t, j) : topk_idx[t][j] = e and assigned_rank[t][j] = r}.
+ * Pairs with an id outside [0, E) or a rank outside [0, G) are skipped.
+ * Nothing is zeroed (counts accumulate). workspace: device scratch of at
+ * least cobalt_replica_load_workspace_bytes(T, K, E, G) bytes, 256-byte
+ * aligned, owned by the caller, contents ignored, not shared by calls that
+ * may overlap; load is updated with plain adds, so overlapping calls must
+ * not share it either.
+ * ---------------------------------------------------------------------- */
+size_t cobalt_replica_load_workspace_bytes(int64_t T, int32_t K, int32_t E, int32_t G);
+
+cobalt_status cobalt_replica_load(const int32_t* topk_idx, const int32_t* assigned_rank,
+                                  int64_t T, int32_t K, int32_t E, int32_t G, uint32_t* load,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Per-step intra-node rebalancing (Section 3.2, Stage 2). Host only,
+ * synchronous, no device memory.
+ *
+ * host_slot_table [G][S] in (as in cobalt_layout_create); host_owner_rank
+ * [E] in or NULL (= lowest rank holding the expert); host_replica_load
+ * [E][G] in: estimated workload of the replica of e on rank r (finite,
+ * >= 0; entries without a replica are ignored).
+ * For each node, the replicas on the node's ranks are sorted by load
+ * (heaviest first; ties by expert id, then by previous rank) and placed one
+ * by one on the least-loaded rank of that node (ties: lowest rank) that has
+ * a free slot and no replica of the same expert. The set of replicas per
+ * node is unchanged. If some replica finds no eligible rank, the node keeps
+ * its previous placement.
+ * host_new_slot_table [G][S] out (may alias nothing else); host_new_owner_rank
+ * [E] out or NULL: the rank the owner replica moved to; host_rank_load [G]
+ * out or NULL: the summed replica load of each rank after placement, in
+ * placement order (fp32).
+ * Returns COBALT_EDATA for an invalid table, owner or load.
+ * ---------------------------------------------------------------------- */
+cobalt_status cobalt_intra_node_rebalance(int32_t N, int32_t gpus_per_node, int32_t E, int32_t S,
+                                          const int32_t* host_slot_table,
+                                          const int32_t* host_owner_rank,
+                                          const float* host_replica_load,
+                                          int32_t* host_new_slot_table,
+                                          int32_t* host_new_owner_rank, float* host_rank_load);
+
+/* ------------------------------------------------------------------------
  * Debug check of routing inputs (synchronous; allocates a few bytes).
  * Checks 0 <= topk_idx < E, distinct experts within each token, and, if
  * src_rank is given, 0 <= src_rank < G and non-decreasing. Returns COBALT_OK

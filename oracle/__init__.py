@@ -60,8 +60,10 @@ def lib():
         L.ref_dispatch.argtypes = [P, P, i64, i32, i32, P, i64, P, P, P, P]
         L.ref_combine.argtypes = [P, i64, P, P, i64, i32, i64, P, P]
         L.ref_traffic.argtypes = [P, P, i64, i32, i32, i32, P, P, P]
+        L.ref_replica_load.argtypes = [P, P, i64, i32, i32, i32, P]
+        L.ref_intra_node_rebalance.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P]
         for f in ("ref_coact_stats", "ref_layout_tables", "ref_assign", "ref_dispatch",
-                  "ref_combine", "ref_traffic"):
+                  "ref_combine", "ref_traffic", "ref_replica_load", "ref_intra_node_rebalance"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -197,3 +199,29 @@ def traffic(assigned, N, g, src=None):
     _check(lib().ref_traffic(_p(assigned), _p(src), T, K, N, g, ctypes.byref(V),
                              ctypes.byref(cp), _p(load)), "traffic")
     return V.value, cp.value, load
+
+
+def replica_load(topk, assigned, E, G, load=None):
+    """Adds into load [E, G] uint32 (fresh if None)."""
+    topk = _c(topk, np.int32)
+    assigned = _c(assigned, np.int32)
+    T, K = topk.shape
+    load = np.zeros((E, G), np.uint32) if load is None else load
+    _check(lib().ref_replica_load(_p(topk), _p(assigned), T, K, E, G, _p(load)), "replica_load")
+    return load
+
+
+def intra_node_rebalance(N, g, E, slot_table, owner, replica_load):
+    """Stage-2 greedy per node. Returns (new_slot [G, S], new_owner [E],
+    rank_load [G] fp32)."""
+    st = _c(slot_table, np.int32)
+    G, S = st.shape
+    own = _c(owner, np.int32)
+    rl = _c(replica_load, np.float32)
+    assert rl.shape == (E, G)
+    out = np.zeros((G, S), np.int32)
+    new_own = np.zeros(E, np.int32)
+    rank_load = np.zeros(G, np.float32)
+    _check(lib().ref_intra_node_rebalance(N, g, E, S, _p(st), _p(own), _p(rl), _p(out),
+                                          _p(new_own), _p(rank_load)), "intra_node_rebalance")
+    return out, new_own, rank_load

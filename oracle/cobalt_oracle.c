@@ -397,3 +397,128 @@ int ref_traffic(const int32_t* assigned, const int32_t* src, int64_t T, int32_t 
     }
     return REF_OK;
 }
+
+/* ---------------------------------------------------------------------- */
+/* Per-replica workload (Section 3.1: w_er, the tasks of expert e executed */
+/* by its replica on rank r). load [E][G] += counts; pairs with an id or   */
+/* rank out of range are skipped.                                          */
+/* ---------------------------------------------------------------------- */
+int ref_replica_load(const int32_t* topk, const int32_t* assigned, int64_t T, int32_t K,
+                     int32_t E, int32_t G, uint32_t* load)
+{
+    if (T < 0 || K < 1 || E < 1 || G < 1) return REF_EINVAL;
+    for (int64_t p = 0; p < T * K; ++p) {
+        int32_t e = topk[p], r = assigned[p];
+        if (e < 0 || e >= E || r < 0 || r >= G) continue;
+        load[(int64_t)e * G + r] += 1u;
+    }
+    return REF_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Per-step intra-node rebalancing (Section 3.2, Stage 2): for each node,  */
+/* sort the node's replicas by estimated workload, heaviest first (ties:   */
+/* smaller expert id, then smaller previous rank), and give each in turn to */
+/* the least-loaded rank of the node (ties: smaller rank) that has a free  */
+/* slot and holds no replica of the same expert. A node where some replica */
+/* finds no such rank keeps its previous placement. rank_load receives the */
+/* fp32 sums of each rank's replica loads in placement order.              */
+/* ---------------------------------------------------------------------- */
+struct ref_rep { float load; int32_t e, r; };
+
+static int rep_before(const struct ref_rep* a, const struct ref_rep* b)
+{
+    if (a->load != b->load) return a->load > b->load;
+    if (a->e != b->e) return a->e < b->e;
+    return a->r < b->r;
+}
+
+int ref_intra_node_rebalance(int32_t N, int32_t g, int32_t E, int32_t S,
+                             const int32_t* slot, const int32_t* owner_in, const float* rload,
+                             int32_t* new_slot, int32_t* new_owner, float* rank_load)
+{
+    int32_t G = N * g;
+    if (N < 1 || g < 1 || E < 1 || S < 1) return REF_EINVAL;
+    uint32_t* node_mask = (uint32_t*)calloc((size_t)E, sizeof(uint32_t));
+    uint32_t* rank_mask = (uint32_t*)calloc((size_t)E * N, sizeof(uint32_t));
+    int32_t* owner = (int32_t*)calloc((size_t)E, sizeof(int32_t));
+    struct ref_rep* reps = (struct ref_rep*)malloc((size_t)g * S * sizeof(struct ref_rep));
+    int32_t* dest = (int32_t*)malloc((size_t)g * S * sizeof(int32_t));
+    float* load = (float*)malloc((size_t)g * sizeof(float));
+    int32_t* used = (int32_t*)malloc((size_t)g * sizeof(int32_t));
+    int rc = REF_OK;
+    if (!node_mask || !rank_mask || !owner || !reps || !dest || !load || !used) {
+        rc = REF_EINVAL;
+        goto done;
+    }
+    rc = ref_layout_tables(N, g, E, S, slot, owner_in, node_mask, rank_mask, owner);
+    if (rc != REF_OK) goto done;
+    for (int32_t r = 0; r < G; ++r)
+        for (int32_t k = 0; k < S; ++k) {
+            int32_t e = slot[r * S + k];
+            if (e < 0) continue;
+            float l = rload[(int64_t)e * G + r];
+            if (!(l >= 0.0f) || isinf(l)) { rc = REF_EDATA; goto done; }
+        }
+    for (int32_t e = 0; e < E; ++e) new_owner[e] = owner[e];
+    for (int32_t n = 0; n < N; ++n) {
+        int32_t nrep = 0;
+        for (int32_t i = 0; i < g; ++i)
+            for (int32_t k = 0; k < S; ++k) {
+                int32_t r = n * g + i, e = slot[r * S + k];
+                if (e < 0) continue;
+                reps[nrep].load = rload[(int64_t)e * G + r];
+                reps[nrep].e = e;
+                reps[nrep].r = r;
+                ++nrep;
+            }
+        /* insertion sort, heaviest first */
+        for (int32_t a = 1; a < nrep; ++a) {
+            struct ref_rep x = reps[a];
+            int32_t b = a - 1;
+            while (b >= 0 && rep_before(&x, &reps[b])) { reps[b + 1] = reps[b]; --b; }
+            reps[b + 1] = x;
+        }
+        for (int32_t i = 0; i < g; ++i) { load[i] = 0.0f; used[i] = 0; }
+        int placed_all = 1;
+        for (int32_t q = 0; q < nrep && placed_all; ++q) {
+            int32_t best = -1;
+            for (int32_t i = 0; i < g; ++i) {
+                int holds = 0;
+                for (int32_t u = 0; u < q; ++u)
+                    if (dest[u] == i && reps[u].e == reps[q].e) holds = 1;
+                if (used[i] >= S || holds) continue;
+                if (best < 0 || load[i] < load[best]) best = i;
+            }
+            if (best < 0) { placed_all = 0; break; }
+            dest[q] = best;
+            load[best] += reps[q].load;
+            used[best] += 1;
+        }
+        if (placed_all) {
+            for (int32_t i = 0; i < g; ++i) {
+                int32_t r = n * g + i, k = 0;
+                for (int32_t q = 0; q < nrep; ++q)
+                    if (dest[q] == i) new_slot[r * S + k++] = reps[q].e;
+                for (; k < S; ++k) new_slot[r * S + k] = -1;
+                if (rank_load) rank_load[r] = load[i];
+            }
+            for (int32_t q = 0; q < nrep; ++q)
+                if (owner[reps[q].e] == reps[q].r) new_owner[reps[q].e] = n * g + dest[q];
+        } else {
+            for (int32_t i = 0; i < g; ++i) {
+                int32_t r = n * g + i;
+                float l = 0.0f;
+                for (int32_t k = 0; k < S; ++k) {
+                    int32_t e = slot[r * S + k];
+                    new_slot[r * S + k] = e;
+                    if (e >= 0) l += rload[(int64_t)e * G + r];
+                }
+                if (rank_load) rank_load[r] = l;
+            }
+        }
+    }
+done:
+    free(node_mask); free(rank_mask); free(owner); free(reps); free(dest); free(load); free(used);
+    return rc;
+}

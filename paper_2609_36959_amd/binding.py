@@ -61,6 +61,9 @@ def lib() -> ctypes.CDLL:
                                  ctypes.c_int),
         "cobalt_combine": ([P, P, P, i64, i32, i64, P, P, P], ctypes.c_int),
         "cobalt_validate_routing": ([P, P, i64, i32, i32, i32, P, P], ctypes.c_int),
+        "cobalt_replica_load_workspace_bytes": ([i64, i32, i32, i32], sz),
+        "cobalt_replica_load": ([P, P, i64, i32, i32, i32, P, P, sz, P], ctypes.c_int),
+        "cobalt_intra_node_rebalance": ([i32, i32, i32, i32, P, P, P, P, P, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -202,6 +205,46 @@ def cobalt_combine(expert_out: torch.Tensor, pos: torch.Tensor, gates: torch.Ten
     _call("cobalt_combine", _dev(expert_out, "expert_out", BF16, (T * K, d)),
           _dev(pos, "pos", I32), _dev(gates, "gates", F32, (T, K)), T, K, d,
           _dev(y, "y", BF16, (T, d)), _dev(y_f32, "y_f32", F32, (T, d)), _stream(stream))
+
+
+def cobalt_replica_load_workspace_bytes(T: int, K: int, E: int, G: int) -> int:
+    return int(lib().cobalt_replica_load_workspace_bytes(T, K, E, G))
+
+
+def cobalt_replica_load(topk_idx: torch.Tensor, assigned_rank: torch.Tensor, E: int, G: int,
+                        load: torch.Tensor, workspace: torch.Tensor, stream=None) -> None:
+    T, K = topk_idx.shape
+    _call("cobalt_replica_load", _dev(topk_idx, "topk_idx", I32),
+          _dev(assigned_rank, "assigned_rank", I32, (T, K)), T, K, E, G,
+          _dev(load, "load", U32, (E, G)), _dev(workspace, "workspace", WS),
+          workspace.numel() * workspace.element_size(), _stream(stream))
+
+
+def cobalt_intra_node_rebalance(N: int, gpus_per_node: int, E: int, S: int, slot_table,
+                                owner_rank, replica_load):
+    """Host-only Stage-2 rebalancing. Returns (new_slot_table [G, S] int32,
+    new_owner_rank [E] int32, rank_load [G] float32)."""
+    G = N * gpus_per_node
+    st = np.ascontiguousarray(slot_table, dtype=np.int32)
+    if st.shape != (G, S):
+        raise ValueError(f"slot_table must be [{G}, {S}]")
+    own = None if owner_rank is None else np.ascontiguousarray(owner_rank, dtype=np.int32)
+    rl = np.ascontiguousarray(replica_load, dtype=np.float32)
+    if rl.shape != (E, G):
+        raise ValueError(f"replica_load must be [{E}, {G}]")
+    out = np.zeros((G, S), np.int32)
+    new_own = np.zeros(E, np.int32)
+    rank_load = np.zeros(G, np.float32)
+    P = ctypes.c_void_p
+    _call("cobalt_intra_node_rebalance", N, gpus_per_node, E, S, st.ctypes.data_as(P),
+          None if own is None else own.ctypes.data_as(P), rl.ctypes.data_as(P),
+          out.ctypes.data_as(P), new_own.ctypes.data_as(P), rank_load.ctypes.data_as(P))
+    return out, new_own, rank_load
+
+
+def replica_load_workspace_for(T: int, K: int, E: int, G: int, device="cuda") -> torch.Tensor:
+    n = cobalt_replica_load_workspace_bytes(T, K, E, G)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
 
 
 def cobalt_validate_routing(topk_idx: torch.Tensor, src_rank: Optional[torch.Tensor], E: int,

@@ -230,6 +230,25 @@ extern "C" cobalt_status cobalt_combine(const void* eo, const int32_t* pos, cons
     return launch_combine(eo, pos, gates, T, K, d, y, y32, (hipStream_t)stream);
 }
 
+extern "C" size_t cobalt_replica_load_workspace_bytes(int64_t T, int32_t K, int32_t E,
+                                                     int32_t G) {
+    if (T < 0 || K < 1 || K > kMaxK || E < 1 || E > kMaxE || G < 1 || G > kMaxG) return 0;
+    return replica_load_workspace_bytes(T, K, E, G);
+}
+
+extern "C" cobalt_status cobalt_replica_load(const int32_t* topk, const int32_t* assigned,
+                                             int64_t T, int32_t K, int32_t E, int32_t G,
+                                             uint32_t* load, void* ws, size_t ws_bytes,
+                                             void* stream) {
+    if (T < 0 || K < 1 || K > kMaxK || E < 1 || E > kMaxE || G < 1 || G > kMaxG) return COBALT_EINVAL;
+    if (!load || !ws || (T > 0 && (!topk || !assigned))) return COBALT_EINVAL;
+    if (((uintptr_t)ws & 255u) != 0) return COBALT_EINVAL;
+    if (T * K >= (int64_t(1) << 31)) return COBALT_EUNSUPPORTED;
+    if (ws_bytes < replica_load_workspace_bytes(T, K, E, G)) return COBALT_EINVAL;
+    if (T == 0) return COBALT_OK;
+    return launch_replica_load(topk, assigned, T, K, E, G, load, ws, ws_bytes, (hipStream_t)stream);
+}
+
 extern "C" cobalt_status cobalt_validate_routing(const int32_t* topk, const int32_t* src,
                                                  int64_t T, int32_t K, int32_t E, int32_t G,
                                                  uint32_t* host_flags, void* stream) {

@@ -53,6 +53,10 @@ cobalt_status launch_dispatch(const int32_t* assigned, const int32_t* src, int64
                               hipStream_t s);
 cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* gates, int64_t T,
                              int K, int64_t d, void* y, float* y32, hipStream_t s);
+size_t replica_load_workspace_bytes(int64_t T, int K, int E, int G);
+cobalt_status launch_replica_load(const int32_t* topk, const int32_t* assigned, int64_t T, int K,
+                                  int E, int G, uint32_t* load, void* ws, size_t ws_bytes,
+                                  hipStream_t s);
 cobalt_status launch_validate(const int32_t* topk, const int32_t* src, int64_t T, int K, int E,
                               int G, uint32_t* dflags, hipStream_t s);
 

@@ -53,6 +53,8 @@ class RoutingStep:
         self.y = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
         self.workspace = B.workspace_for(T, K, G, device=dev)
         self.stats_workspace = B.stats_workspace_for(T, K, E, device=dev)
+        self.replica_load = torch.zeros(E, G, dtype=torch.int32, device=dev)
+        self.load_workspace = B.replica_load_workspace_for(T, K, E, G, device=dev)
 
     def set_routing(self, step: int, route_device=None):
         rd = self.device if route_device is None else route_device
@@ -82,6 +84,11 @@ class RoutingStep:
 
     def combine(self, y_f32=None, stream=None):
         B.cobalt_combine(self.eo, self.pos, self.gates, self.y, y_f32, stream=stream)
+
+    def load(self, stream=None):
+        """Adds this step's per-replica task counts w_er into replica_load."""
+        B.cobalt_replica_load(self.topk, self.assigned, self.w.E, self.w.G, self.replica_load,
+                              self.load_workspace, stream=stream)
 
     def run(self, mode=0, stream=None):
         self.stats(stream)

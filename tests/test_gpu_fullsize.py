@@ -73,9 +73,12 @@ def test_full_size_single_step(name):
     print(f"full size {name} {w.describe()}", flush=True)
     st = PL.RoutingStep(w, seed=w.seed, device="cuda")
     st.run()
+    st.load()
     torch.cuda.synchronize()
     tabs = oracle.layout_tables(w.N, w.g, w.E, st.table, st.owner)
     check_step(st, tabs, None, None, np.random.default_rng(w.seed))
+    ref = oracle.replica_load(st.topk.cpu().numpy(), st.assigned.cpu().numpy(), w.E, w.G)
+    assert np.array_equal(st.replica_load.cpu().numpy().view(np.uint32), ref)
     round_trip(st)
     st.close()
     del st

@@ -268,3 +268,36 @@ def test_round_trip_returns_x():
     torch.cuda.synchronize()
     assert torch.equal(st.y.float(), st.x.float())
     st.close()
+
+
+@pytest.mark.parametrize("name,T", [("tiny", 4096), ("clusters-e64", 5003), ("drift-e384", 64 * 50),
+                                    ("colocate-e256", 64 * 300 + 7)])
+def test_replica_load_matches_oracle(name, T):
+    """Per-replica task counts w_er (Section 3.1) from the assignment."""
+    w = W.with_sizes(W.WORKLOADS[name], T=T)
+    topk, _ = W.routing(w, w.seed)
+    table, owner = W.layout(w, w.seed)
+    src = W.ragged_src(T, w.G, seed=1)
+    tabs = oracle.layout_tables(w.N, w.g, w.E, table, owner)
+    a, _ = oracle.assign(w.N, w.g, w.E, tabs, topk.numpy(), src, seed=2)
+    a[0, 0] = -1  # out-of-range ranks are skipped
+    load = torch.zeros(w.E, w.G, dtype=torch.int32, device="cuda")
+    ws = B.replica_load_workspace_for(T, w.K, w.E, w.G)
+    ws.fill_(0x5A)
+    B.cobalt_replica_load(dev_i32(topk.numpy()), dev_i32(a), w.E, w.G, load, ws)
+    B.cobalt_replica_load(dev_i32(topk.numpy()), dev_i32(a), w.E, w.G, load, ws)
+    ref = oracle.replica_load(topk.numpy(), a, w.E, w.G)
+    ref = oracle.replica_load(topk.numpy(), a, w.E, w.G, ref)
+    assert np.array_equal(u32(load), ref)
+
+
+def test_replica_load_many_bands():
+    """E * G beyond one LDS band (E = 4096, G = 32)."""
+    rng = np.random.default_rng(4)
+    T, K, E, G = 3000, 8, 4096, 32
+    topk = rng.integers(0, E, size=(T, K)).astype(np.int32)
+    a = rng.integers(0, G, size=(T, K)).astype(np.int32)
+    load = torch.zeros(E, G, dtype=torch.int32, device="cuda")
+    B.cobalt_replica_load(dev_i32(topk), dev_i32(a), E, G, load,
+                          B.replica_load_workspace_for(T, K, E, G))
+    assert np.array_equal(u32(load), oracle.replica_load(topk, a, E, G))
