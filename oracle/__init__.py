@@ -58,12 +58,13 @@ def lib():
         L.ref_layout_tables.argtypes = [i32, i32, i32, i32, P, P, P, P, P]
         L.ref_assign.argtypes = [i32, i32, i32, P, P, P, P, P, i64, i32, u64, u64, i32, P, P]
         L.ref_dispatch.argtypes = [P, P, i64, i32, i32, P, i64, P, P, P, P]
+        L.ref_node_dispatch.argtypes = [P, P, i64, i32, i32, i32, P, i64, P, P, P, P, P, P]
         L.ref_combine.argtypes = [P, i64, P, P, i64, i32, i64, P, P]
         L.ref_traffic.argtypes = [P, P, i64, i32, i32, i32, P, P, P]
         L.ref_replica_load.argtypes = [P, P, i64, i32, i32, i32, P]
         L.ref_intra_node_rebalance.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P]
         for f in ("ref_coact_stats", "ref_layout_tables", "ref_assign", "ref_dispatch",
-                  "ref_combine", "ref_traffic", "ref_replica_load", "ref_intra_node_rebalance"):
+                  "ref_node_dispatch", "ref_combine", "ref_traffic", "ref_replica_load", "ref_intra_node_rebalance"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -171,6 +172,33 @@ def dispatch(assigned, G, src=None, x=None, d=0):
     _check(lib().ref_dispatch(_p(assigned), _p(src), T, K, G, _p(x), d, _p(counts),
                               _p(offsets), _p(pos), _p(packed)), "dispatch")
     return counts, offsets, pos, packed
+
+
+def node_dispatch(assigned, N, g, src=None, x=None, d=0):
+    """Node-deduplicated layout. Returns (counts [G, N] i32, offsets [G*N+1]
+    i64, node_pos [T, N] i32, fwd [rows] u32, row_token [rows] i32, packed
+    [rows, d] u16 or None), trimmed to the rows actually used."""
+    assigned = _c(assigned, np.int32)
+    T, K = assigned.shape
+    G = N * g
+    src = _c(src, np.int32)
+    cap = T * min(K, N)
+    counts = np.zeros((G, N), np.int32)
+    offsets = np.zeros(G * N + 1, np.int64)
+    node_pos = np.zeros((T, N), np.int32)
+    fwd = np.zeros(max(cap, 1), np.uint32)
+    row_token = np.zeros(max(cap, 1), np.int32)
+    packed = None
+    if x is not None:
+        x = _c(x, np.uint16)
+        d = x.shape[1]
+        packed = np.zeros((max(cap, 1), d), np.uint16)
+    _check(lib().ref_node_dispatch(_p(assigned), _p(src), T, K, N, g, _p(x), d, _p(counts),
+                                   _p(offsets), _p(node_pos), _p(fwd), _p(row_token),
+                                   _p(packed)), "node_dispatch")
+    rows = int(offsets[-1])
+    return (counts, offsets, node_pos, fwd[:rows], row_token[:rows],
+            None if packed is None else packed[:rows])
 
 
 def combine(expert_out, pos, gates):

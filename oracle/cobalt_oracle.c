@@ -344,6 +344,89 @@ int ref_dispatch(const int32_t* assigned, const int32_t* src, int64_t T, int32_t
 }
 
 /* ---------------------------------------------------------------------- */
+/* Node-deduplicated dispatch layout (Section 1 and Section 3.1: a token  */
+/* crosses to a node once, however many ranks there need it, and is then  */
+/* forwarded inside that node). Token t has one row per distinct node     */
+/*   n in { node(r_tj) : j = 0..K-1 },                                    */
+/* its own node included, so the rows whose node differs from node(s_t)   */
+/* number exactly the V of Eq. 1. Bucket of row (t, n) = (s_t, n), in      */
+/* row-major order over [G][N]; a bucket keeps its rows in increasing t.   */
+/*   counts [G][N]      rows per (source rank, destination node)           */
+/*   offsets [G*N+1]    exclusive prefix sum of counts, offsets[G*N]=total */
+/*   node_pos [T][N]    row of (t, n), or -1 if no slot of t goes to n     */
+/*   fwd [rows]         forwarding mask of the row: bit i set iff some     */
+/*                      slot of its token is assigned to rank n*g + i      */
+/*   row_token [rows]   t of the row (nullable)                            */
+/*   packed [rows][d]   packed[row] = x[t] (bf16 bits), nullable           */
+/* rows <= T * min(K, N).                                                  */
+/* ---------------------------------------------------------------------- */
+int ref_node_dispatch(const int32_t* assigned, const int32_t* src, int64_t T, int32_t K,
+                      int32_t N, int32_t g, const uint16_t* x, int64_t d,
+                      int32_t* counts, int64_t* offsets, int32_t* node_pos, uint32_t* fwd,
+                      int32_t* row_token, uint16_t* packed)
+{
+    if (T < 0 || K < 1 || N < 1 || N > 32 || g < 1 || g > 32 || d < 0) return REF_EINVAL;
+    int32_t G = N * g;
+    if (!src && T % G != 0) return REF_EINVAL;
+    int64_t GN = (int64_t)G * N;
+    uint32_t* mask = (uint32_t*)malloc((size_t)N * sizeof(uint32_t));
+    int64_t* cursor = (int64_t*)malloc((size_t)(GN > 0 ? GN : 1) * sizeof(int64_t));
+    if (!mask || !cursor) {
+        free(mask);
+        free(cursor);
+        return REF_EINVAL;
+    }
+    int rc = REF_OK;
+    for (int64_t b = 0; b < GN; ++b) counts[b] = 0;
+    /* pass 1: which nodes each token reaches */
+    for (int64_t t = 0; t < T && rc == REF_OK; ++t) {
+        int32_t s = src_of(src, t, T, G);
+        if (s < 0 || s >= G) rc = REF_EDATA;
+        for (int32_t n = 0; n < N; ++n) mask[n] = 0;
+        for (int32_t j = 0; j < K && rc == REF_OK; ++j) {
+            int32_t r = assigned[t * K + j];
+            if (r < 0 || r >= G) rc = REF_EDATA;
+            else mask[r / g] |= 1u << (r % g);
+        }
+        for (int32_t n = 0; n < N && rc == REF_OK; ++n)
+            if (mask[n]) counts[(int64_t)s * N + n] += 1;
+    }
+    if (rc == REF_OK) {
+        int64_t run = 0;
+        for (int64_t b = 0; b < GN; ++b) {
+            offsets[b] = run;
+            run += counts[b];
+        }
+        offsets[GN] = run;
+        for (int64_t b = 0; b < GN; ++b) cursor[b] = offsets[b];
+        /* pass 2: rows in increasing t within each bucket */
+        for (int64_t t = 0; t < T; ++t) {
+            int32_t s = src_of(src, t, T, G);
+            for (int32_t n = 0; n < N; ++n) mask[n] = 0;
+            for (int32_t j = 0; j < K; ++j) {
+                int32_t r = assigned[t * K + j];
+                mask[r / g] |= 1u << (r % g);
+            }
+            for (int32_t n = 0; n < N; ++n) {
+                if (!mask[n]) {
+                    node_pos[t * N + n] = -1;
+                    continue;
+                }
+                int64_t row = cursor[(int64_t)s * N + n]++;
+                node_pos[t * N + n] = (int32_t)row;
+                fwd[row] = mask[n];
+                if (row_token) row_token[row] = (int32_t)t;
+                if (packed)
+                    for (int64_t c = 0; c < d; ++c) packed[row * d + c] = x[t * d + c];
+            }
+        }
+    }
+    free(mask);
+    free(cursor);
+    return rc;
+}
+
+/* ---------------------------------------------------------------------- */
 /* Combine and weighted sum (Fig. 1, last stage): token t gets            */
 /*   y[t][c] = bf16( sum_j gates[t][j] * expert_out[pos[t][j]][c] )       */
 /* accumulated in fp32 from 0, one fused multiply-add per slot, j = 0..K-1.*/
