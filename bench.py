@@ -29,7 +29,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK = 8.0e12  # MI355X HBM3E, bytes/s
 METRIC = "routed tokens/sec (stats+assign+pack+combine), % of HBM peak, 1 MI355X"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_{call}_{workload}.txt")
-KERNEL_SOURCES = {"cobalt_dispatch_pack": "dispatch.hip", "cobalt_combine": "combine.hip"}
+KERNEL_SOURCES = {"cobalt_dispatch_pack": "dispatch.hip", "cobalt_combine": "combine.hip",
+                  "cobalt_node_dispatch_pack": "dispatch.hip"}
 
 
 def parse():
@@ -56,6 +57,14 @@ def algorithmic_bytes(w):
         "cobalt_dispatch_pack": T * d * 2 + T * K * d * 2 + T * K * 8 + 12 * G * G,
         "cobalt_combine": T * K * d * 2 + T * K * 8 + T * d * 2,
     }
+
+
+def node_dispatch_bytes(w, rows):
+    """Bytes the node-deduplicated dispatch must move for `rows` node rows:
+    read the assignment and x once, write the packed rows, node_pos, the
+    forwarding masks and row tokens, and the [G][N] counts and offsets."""
+    T, K, d, N, G = w.T, w.K, w.d, w.N, w.G
+    return T * K * 4 + T * d * 2 + rows * d * 2 + T * N * 4 + rows * 8 + 12 * G * N
 
 
 def source_digest(call):
@@ -321,6 +330,30 @@ def main():
         ev[1].record(stream)
     torch.cuda.synchronize()
     result["extra_calls_ms"] = {"cobalt_replica_load": ev[0].elapsed_time(ev[1]) / args.steps}
+    # the node-deduplicated dispatch of the last step's assignment: one row
+    # per (token, destination node) instead of one per (token, expert)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    with torch.cuda.stream(stream):
+        st.node_pack(stream=stream)
+        ev[0].record(stream)
+        for _ in range(args.steps):
+            st.node_pack(stream=stream)
+        ev[1].record(stream)
+    torch.cuda.synchronize()
+    node_ms = ev[0].elapsed_time(ev[1]) / args.steps
+    rows = int(st.node_offsets[-1].item())
+    home = (torch.arange(w.T, device="cuda") // (w.T // w.G)) // w.g if st.src is None \
+        else st.src.long() // w.g
+    local_rows = int((st.node_pos.gather(1, home.long()[:, None]) >= 0).sum().item())
+    nb = node_dispatch_bytes(w, rows)
+    result["extra_calls_ms"]["cobalt_node_dispatch_pack"] = node_ms
+    result["node_dedup_dispatch"] = {
+        "rows": rows, "rows_per_token": rows / w.T, "cross_node_rows": rows - local_rows,
+        "rows_vs_pair_layout": rows / (w.T * w.K),
+        "algorithmic_bytes": nb, "achieved_gbps": nb / (node_ms * 1e-3) / 1e9,
+        "hbm_frac": nb / (node_ms * 1e-3) / HBM_PEAK,
+        "traffic": measured_traffic("cobalt_node_dispatch_pack", wl_name),
+        "pair_pack_ms": call_ms["cobalt_dispatch_pack"], "node_pack_ms": node_ms}
     result["routing"] = routing_quality(st, torch, B, W)
     result["routing"]["stage2_rebalance"] = stage2_demo(st, torch, B, W)
     if not args.no_cpu_baseline:

@@ -160,6 +160,45 @@ cobalt_status cobalt_dispatch_pack(const int32_t* assigned_rank, const int32_t* 
                                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Step 3': node-deduplicated dispatch layout and pack (Section 1 and
+ * Section 3.1, Eq. 1: a token crosses to a node once, however many ranks
+ * there need it, and is then forwarded inside the node).
+ *
+ * Token t has one row per distinct node n among { node(r_tj) }, its own
+ * node included, so the rows whose node differs from node(s_t) number
+ * exactly Eq. 1's V. Bucket of row (t, n): (s_t, n), buckets in row-major
+ * order over [G][N]; each bucket keeps its rows in increasing t.
+ * assigned_rank [T][K] int32 in; src_rank as in cobalt_assign; G = N *
+ *   gpus_per_node.
+ * x [T][d] bf16 in (may be NULL together with packed: layout only).
+ * node_counts [G][N] int32 out: rows per (source rank, destination node).
+ * node_offsets [G*N+1] int64 out: exclusive prefix sum of node_counts,
+ *   node_offsets[G*N] = number of rows.
+ * node_pos [T][N] int32 out: row of (t, n), -1 if no slot of t goes to n.
+ * fwd_mask [rows] uint32 out: the intra-node forwarding index; bit i is set
+ *   iff some slot of the row's token is assigned to rank n*gpus_per_node+i.
+ * row_token [rows] int32 out (may be NULL): token of each row.
+ * packed [rows][d] bf16 out: packed[node_pos[t][n]] = x[t], bit for bit.
+ * fwd_mask, row_token and packed must hold T * min(K, N) rows, the most a
+ *   call can produce.
+ * workspace: device scratch of at least
+ *   cobalt_node_dispatch_workspace_bytes(T, N, gpus_per_node) bytes,
+ *   256-byte aligned, owned by the caller; contents on entry are ignored;
+ *   it must not be shared by calls that may overlap.
+ * Slots with a rank outside [0, G) are skipped; such data is rejected by
+ * cobalt_validate_routing.
+ * ---------------------------------------------------------------------- */
+size_t cobalt_node_dispatch_workspace_bytes(int64_t T, int32_t N, int32_t gpus_per_node);
+
+cobalt_status cobalt_node_dispatch_pack(const int32_t* assigned_rank, const int32_t* src_rank,
+                                        int64_t T, int32_t K, int32_t N, int32_t gpus_per_node,
+                                        const void* x, int64_t d,
+                                        int32_t* node_counts, int64_t* node_offsets,
+                                        int32_t* node_pos, uint32_t* fwd_mask,
+                                        int32_t* row_token, void* packed,
+                                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Step 4: combine and weighted sum (Fig. 1, last stage).
  *
  * expert_out [T*K][d] bf16 in, in the packed layout (row pos[p] holds the

@@ -59,6 +59,9 @@ def lib() -> ctypes.CDLL:
         "cobalt_dispatch_workspace_bytes": ([i64, i32, i32], sz),
         "cobalt_dispatch_pack": ([P, P, i64, i32, i32, P, i64, P, P, P, P, P, sz, P],
                                  ctypes.c_int),
+        "cobalt_node_dispatch_workspace_bytes": ([i64, i32, i32], sz),
+        "cobalt_node_dispatch_pack": ([P, P, i64, i32, i32, i32, P, i64, P, P, P, P, P, P, P, sz,
+                                       P], ctypes.c_int),
         "cobalt_combine": ([P, P, P, i64, i32, i64, P, P, P], ctypes.c_int),
         "cobalt_validate_routing": ([P, P, i64, i32, i32, i32, P, P], ctypes.c_int),
         "cobalt_replica_load_workspace_bytes": ([i64, i32, i32, i32], sz),
@@ -198,6 +201,35 @@ def cobalt_dispatch_pack(assigned_rank: torch.Tensor, src_rank: Optional[torch.T
           workspace.numel() * workspace.element_size(), _stream(stream))
 
 
+def cobalt_node_dispatch_workspace_bytes(T: int, N: int, gpus_per_node: int) -> int:
+    return int(lib().cobalt_node_dispatch_workspace_bytes(T, N, gpus_per_node))
+
+
+def cobalt_node_dispatch_pack(assigned_rank: torch.Tensor, src_rank: Optional[torch.Tensor],
+                              N: int, gpus_per_node: int, x: Optional[torch.Tensor],
+                              node_counts: torch.Tensor, node_offsets: torch.Tensor,
+                              node_pos: torch.Tensor, fwd_mask: torch.Tensor,
+                              row_token: Optional[torch.Tensor], packed: Optional[torch.Tensor],
+                              workspace: torch.Tensor, stream=None) -> None:
+    """fwd_mask, row_token and packed hold T * min(K, N) rows."""
+    T, K = assigned_rank.shape
+    G = N * gpus_per_node
+    cap = T * min(K, N)
+    d = 0 if x is None else x.shape[1]
+    if x is not None:
+        _dev(x, "x", BF16, (T, d))
+    _call("cobalt_node_dispatch_pack", _dev(assigned_rank, "assigned_rank", I32),
+          _dev(src_rank, "src_rank", I32, (T,)), T, K, N, gpus_per_node, _dev(x, "x", BF16), d,
+          _dev(node_counts, "node_counts", I32, (G, N)),
+          _dev(node_offsets, "node_offsets", I64, (G * N + 1,)),
+          _dev(node_pos, "node_pos", I32, (T, N)),
+          _dev(fwd_mask, "fwd_mask", U32, (cap,)),
+          _dev(row_token, "row_token", I32, (cap,)),
+          _dev(packed, "packed", BF16, None if packed is None else (cap, d)),
+          _dev(workspace, "workspace", WS),
+          workspace.numel() * workspace.element_size(), _stream(stream))
+
+
 def cobalt_combine(expert_out: torch.Tensor, pos: torch.Tensor, gates: torch.Tensor,
                    y: torch.Tensor, y_f32: Optional[torch.Tensor] = None, stream=None) -> None:
     T, K = pos.shape
@@ -263,6 +295,12 @@ def cobalt_validate_routing(topk_idx: torch.Tensor, src_rank: Optional[torch.Ten
 def workspace_for(T: int, K: int, G: int, device="cuda") -> torch.Tensor:
     """A dispatch workspace of the size the library asks for."""
     n = cobalt_dispatch_workspace_bytes(T, K, G)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+
+
+def node_workspace_for(T: int, N: int, gpus_per_node: int, device="cuda") -> torch.Tensor:
+    """A node-deduplicated dispatch workspace of the size the library asks for."""
+    n = cobalt_node_dispatch_workspace_bytes(T, N, gpus_per_node)
     return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
 
 

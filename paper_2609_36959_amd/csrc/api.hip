@@ -218,6 +218,34 @@ extern "C" cobalt_status cobalt_dispatch_pack(const int32_t* assigned, const int
                            (hipStream_t)stream);
 }
 
+extern "C" size_t cobalt_node_dispatch_workspace_bytes(int64_t T, int32_t N, int32_t gpn) {
+    if (T < 0 || N < 1 || N > kMaxN || gpn < 1 || gpn > kMaxGpn || N * gpn > kMaxG) return 0;
+    return node_dispatch_workspace_bytes(T, N, N * gpn);
+}
+
+extern "C" cobalt_status cobalt_node_dispatch_pack(const int32_t* assigned, const int32_t* src,
+                                                   int64_t T, int32_t K, int32_t N, int32_t gpn,
+                                                   const void* x, int64_t d, int32_t* counts,
+                                                   int64_t* offsets, int32_t* node_pos,
+                                                   uint32_t* fwd, int32_t* row_token,
+                                                   void* packed, void* ws, size_t ws_bytes,
+                                                   void* stream) {
+    if (T < 0 || K < 1 || K > kMaxK || N < 1 || N > kMaxN || gpn < 1 || gpn > kMaxGpn)
+        return COBALT_EINVAL;
+    const int32_t G = N * gpn;
+    if (G > kMaxG) return COBALT_EUNSUPPORTED;
+    if (!counts || !offsets || !ws) return COBALT_EINVAL;
+    if (T > 0 && (!assigned || !node_pos || !fwd)) return COBALT_EINVAL;
+    if ((x == nullptr) != (packed == nullptr)) return COBALT_EINVAL;
+    if (x && (d < 8 || d % 8 != 0 || !aligned16(x) || !aligned16(packed))) return COBALT_EINVAL;
+    if (((uintptr_t)ws & 255u) != 0) return COBALT_EINVAL;
+    if (T * K >= (int64_t(1) << 31)) return COBALT_EUNSUPPORTED;
+    if (!src && T % G != 0) return COBALT_EINVAL;
+    if (ws_bytes < node_dispatch_workspace_bytes(T, N, G)) return COBALT_EINVAL;
+    return launch_node_dispatch(assigned, src, T, K, N, gpn, x, x ? d : 0, counts, offsets,
+                                node_pos, fwd, row_token, packed, ws, (hipStream_t)stream);
+}
+
 extern "C" cobalt_status cobalt_combine(const void* eo, const int32_t* pos, const float* gates,
                                         int64_t T, int32_t K, int64_t d, void* y, float* y32,
                                         void* stream) {

@@ -21,6 +21,14 @@
 //          over predecessor tiles per destination, then pos
 //   copy   each wave reads a 1-2 KiB slice of one token row of x once
 //          into registers and stores it to the token's K packed rows
+//
+// The node-deduplicated layout (Section 1, Eq. 1: a token crosses to a node
+// once and is forwarded inside it) has one row per (token, destination node)
+// in buckets (source rank, node). A token has at most one row per bucket, so
+//     node_pos[t][n] = offsets[s][n] - colprefix[s][n] + prefix_n(t),
+// where prefix_n(t) counts the tokens before t that reach node n: an N-way
+// prefix count over tokens, done with ballots per node bit and the same
+// decoupled look-back. The same init, scan and copy kernels serve both.
 #include <algorithm>
 
 #include "internal.hpp"
@@ -41,6 +49,8 @@ constexpr uint64_t kFlagAgg = 1ull << 62;
 constexpr uint64_t kFlagInc = 2ull << 62;
 constexpr uint64_t kFlagMask = 3ull << 62;
 constexpr int kCopyWaves = 4;
+constexpr int kNodeChunks = 2;
+constexpr int64_t kNodeTile = (int64_t)kRankWaves * 64 * kNodeChunks;  // tokens per tile
 
 struct Workspace {
     uint32_t* ctrl;    // [0] = next tile id
@@ -51,22 +61,32 @@ struct Workspace {
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
-Workspace carve(void* ws, int64_t T, int K, int G) {
+// ntiles tiles of look-back state over C columns, base[G][C].
+Workspace carve(void* ws, int64_t ntiles, int G, int C) {
     Workspace w;
     char* p = (char*)ws;
-    w.ntiles = (T * K + kTile - 1) / kTile;
+    w.ntiles = ntiles;
     w.ctrl = (uint32_t*)p;
     p += 256;
     w.base = (int32_t*)p;
-    p += align256(sizeof(int32_t) * (size_t)G * G);
+    p += align256(sizeof(int32_t) * (size_t)G * C);
     w.status = (uint64_t*)p;
     return w;
+}
+
+size_t carve_bytes(int64_t ntiles, int G, int C) {
+    return 256 + align256(sizeof(int32_t) * (size_t)G * C) +
+           align256(sizeof(uint64_t) * (size_t)std::max<int64_t>(ntiles, 1) * C);
 }
 
 __device__ __forceinline__ int src_of(const int32_t* src, int64_t t, int64_t tok_per_src) {
     return src ? src[t] : (int)(t / tok_per_src);
 }
 
+// kNode (here and on scan_kernel and copy_kernel) changes no instruction: it
+// gives the node-deduplicated layout's launches kernel names of their own,
+// so per-kernel profiles attribute each launch to its entry point.
+template <bool kNode>
 __global__ __launch_bounds__(kInitThreads) void init_kernel(int32_t* counts, int64_t ncounts,
                                                             uint32_t* ctrl, uint64_t* status,
                                                             int64_t nstatus) {
@@ -134,15 +154,18 @@ __device__ int64_t block_exclusive_scan(int64_t v, int64_t* total) {
     return before;
 }
 
-// With G*G <= kScanLds the counts and offsets are staged in LDS, so the
-// sequential column pass reads LDS instead of global memory.
-template <bool kLds>
+// Exclusive scan of a [R][C] count matrix in row-major order, and
+// base[s][c] = offsets[s][c] - sum_{s' < s} counts[s'][c]. With R*C <=
+// kScanLds the counts and offsets are staged in LDS, so the sequential
+// column pass reads LDS instead of global memory.
+template <bool kLds, bool kNode>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __restrict__ counts,
-                                                            int G, int64_t* __restrict__ offsets,
+                                                            int R, int C,
+                                                            int64_t* __restrict__ offsets,
                                                             int32_t* __restrict__ base) {
     __shared__ int32_t c_lds[kLds ? kScanLds : 1];
     __shared__ int32_t o_lds[kLds ? kScanLds : 1];
-    const int64_t n = (int64_t)G * G;
+    const int64_t n = (int64_t)R * C;
     if (kLds) {
         for (int64_t b = threadIdx.x; b < n; b += kScanThreads) c_lds[b] = counts[b];
         __syncthreads();
@@ -161,10 +184,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __res
     }
     if (threadIdx.x == 0) offsets[n] = total;
     __syncthreads();
-    for (int r = threadIdx.x; r < G; r += kScanThreads) {
+    for (int c = threadIdx.x; c < C; c += kScanThreads) {
         int64_t col = 0;
-        for (int s = 0; s < G; ++s) {
-            const int64_t b = (int64_t)s * G + r;
+        for (int r = 0; r < R; ++r) {
+            const int64_t b = (int64_t)r * C + c;
             base[b] = (int32_t)((kLds ? (int64_t)o_lds[b] : offsets[b]) - col);
             col += cnt(b);
         }
@@ -281,7 +304,7 @@ __global__ __launch_bounds__(kRankThreads) void rank_kernel(
 // write rate than non-temporal ones on this access pattern.
 // KC = compile-time K (0: any K up to 16); with KC the scalar loads of the
 // token's pos entries are issued together.
-template <int CG, int KC>
+template <int CG, int KC, bool kNode>
 __global__ __launch_bounds__(kCopyWaves * 64) void copy_kernel(
     const u32x4* __restrict__ x, const int32_t* __restrict__ pos, int64_t T, int Kr, int64_t nch,
     int64_t TK, u32x4* __restrict__ packed) {
@@ -312,31 +335,250 @@ __global__ __launch_bounds__(kCopyWaves * 64) void copy_kernel(
     }
 }
 
+
+// Node set of one token, for the node-deduplicated layout: code[j] =
+// (node << 8) | index of the rank inside its node, or -1 for a slot with no
+// valid rank; the result has bit n set if some slot goes to node n.
+template <int KM>
+__device__ __forceinline__ uint32_t token_nodes(const int32_t* __restrict__ assigned, int64_t t,
+                                                int K, int g, int G, int (&code)[KM]) {
+    uint32_t B = 0;
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        int cd = -1;
+        if (j < K) {
+            const int r = assigned[t * K + j];
+            if (r >= 0 && r < G) {
+                const int n = r / g;
+                cd = (n << 8) | (r - n * g);
+                B |= 1u << n;
+            }
+        }
+        code[j] = cd;
+    }
+    return B;
+}
+
+// node_counts[s][n]: tokens of source s with a slot on node n (LDS window
+// over the block's sources, global atomics to flush). One token per thread.
+template <int KC>
+__global__ __launch_bounds__(kCountThreads) void node_count_kernel(
+    const int32_t* __restrict__ assigned, const int32_t* __restrict__ src, int64_t T, int Kr,
+    int N, int g, int64_t tok_per_src, int64_t tok_per_blk, int32_t* __restrict__ counts) {
+    constexpr int KM = KC ? KC : kMaxK;
+    const int K = KC ? KC : Kr;
+    const int G = N * g;
+    __shared__ uint32_t h[kCountWin];
+    const int64_t t0 = (int64_t)blockIdx.x * tok_per_blk;
+    const int64_t t1 = min(T, t0 + tok_per_blk);
+    if (t0 >= t1) return;
+    const int s_lo = src_of(src, t0, tok_per_src);
+    const int s_hi = src_of(src, t1 - 1, tok_per_src);
+    const bool win = s_lo >= 0 && s_hi < G && s_hi >= s_lo && (s_hi - s_lo + 1) * N <= kCountWin;
+    const int nwin = win ? (s_hi - s_lo + 1) * N : 0;
+    for (int i = threadIdx.x; i < nwin; i += kCountThreads) h[i] = 0;
+    __syncthreads();
+    for (int64_t t = t0 + threadIdx.x; t < t1; t += kCountThreads) {
+        const int s = src_of(src, t, tok_per_src);
+        if (s < 0 || s >= G) continue;
+        int code[KM];
+        uint32_t B = token_nodes<KM>(assigned, t, K, g, G, code);
+        const bool in_win = win && s >= s_lo && s <= s_hi;
+        while (B) {
+            const int n = __ffs(B) - 1;
+            B &= B - 1;
+            if (in_win)
+                atomicAdd(&h[(s - s_lo) * N + n], 1u);
+            else
+                atomicAdd(&counts[(int64_t)s * N + n], 1);
+        }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < nwin; i += kCountThreads) {
+        const uint32_t v = h[i];
+        if (v) atomicAdd(&counts[(int64_t)s_lo * N + i], (int32_t)v);
+    }
+}
+
+// Per tile of kNodeTile tokens: each (wave, chunk) segment of 64 tokens
+// counts its tokens per node with one ballot per node, the segments are
+// scanned in token order in LDS, the tile's per-node totals go through the
+// decoupled look-back, and each (token, node) row gets
+//     base[s][n] + tile prefix + segment prefix + lanes below with bit n.
+// node_pos is written for every (t, n), -1 where the token has no row.
+template <int KC>
+__global__ __launch_bounds__(kRankThreads) void node_rank_kernel(
+    const int32_t* __restrict__ assigned, const int32_t* __restrict__ src, int64_t T, int Kr,
+    int N, int g, int64_t tok_per_src, int64_t ntiles, uint32_t* __restrict__ ctrl,
+    const int32_t* __restrict__ base, uint64_t* __restrict__ status,
+    int32_t* __restrict__ node_pos, uint32_t* __restrict__ fwd, int32_t* __restrict__ row_token) {
+    constexpr int KM = KC ? KC : kMaxK;
+    constexpr int kSegs = kRankWaves * kNodeChunks;
+    const int K = KC ? KC : Kr;
+    const int G = N * g;
+    __shared__ uint32_t seg[kSegs][kMaxN];  // segment counts, then segment prefixes
+    __shared__ uint32_t tile_excl[kMaxN];
+    __shared__ int tile_sh;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+
+    if (threadIdx.x == 0) tile_sh = (int)atomicAdd(ctrl, 1u);
+    __syncthreads();
+    const int64_t tile = tile_sh;
+    if (tile >= ntiles) return;
+
+    const uint64_t lt_mask = (1ull << lane) - 1ull;
+    const int64_t t_wave = tile * kNodeTile + (int64_t)wave * 64 * kNodeChunks;
+    int code[kNodeChunks][KM];
+    uint32_t nodes[kNodeChunks];
+    int ss[kNodeChunks];
+#pragma unroll
+    for (int c = 0; c < kNodeChunks; ++c) {
+        const int64_t t = t_wave + c * 64 + lane;
+        const int s = t < T ? src_of(src, t, tok_per_src) : -1;
+        uint32_t B = 0;
+        if (s >= 0 && s < G) {
+            B = token_nodes<KM>(assigned, t, K, g, G, code[c]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < KM; ++j) code[c][j] = -1;
+        }
+        nodes[c] = B;
+        ss[c] = s;
+        uint32_t mine = 0;  // lane n keeps the segment's count for node n
+        for (int n = 0; n < N; ++n) {
+            const uint32_t cnt = (uint32_t)__popcll(__ballot((B >> n) & 1u));
+            if (lane == n) mine = cnt;
+        }
+        if (lane < N) seg[wave * kNodeChunks + c][lane] = mine;
+    }
+    __syncthreads();
+    if (threadIdx.x < N) {
+        const int n = threadIdx.x;
+        uint32_t agg = 0;
+        for (int q = 0; q < kSegs; ++q) {
+            const uint32_t v = seg[q][n];
+            seg[q][n] = agg;
+            agg += v;
+        }
+        uint64_t* mine = status + tile * N + n;
+        uint32_t excl = 0;
+        if (tile == 0) {
+            st_status(mine, kFlagInc | agg);
+        } else {
+            st_status(mine, kFlagAgg | agg);
+            int64_t q = tile - 1;
+            for (;;) {
+                const uint64_t v = ld_status(status + q * N + n);
+                const uint64_t f = v & kFlagMask;
+                if (f == 0) {
+                    __builtin_amdgcn_s_sleep(1);
+                    continue;
+                }
+                excl += (uint32_t)v;
+                if (f == kFlagInc) break;
+                --q;
+            }
+            st_status(mine, kFlagInc | (uint64_t)(excl + agg));
+        }
+        tile_excl[n] = excl;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < kNodeChunks; ++c) {
+        const int64_t t = t_wave + c * 64 + lane;
+        const uint32_t B = nodes[c];
+        const int q = wave * kNodeChunks + c;
+        for (int n = 0; n < N; ++n) {
+            const bool bit = (B >> n) & 1u;
+            const uint64_t bal = __ballot(bit);
+            if (t < T) {
+                int32_t row = -1;
+                if (bit) {
+                    row = base[(int64_t)ss[c] * N + n] + (int)tile_excl[n] + (int)seg[q][n] +
+                          __popcll(bal & lt_mask);
+                    uint32_t m = 0;
+#pragma unroll
+                    for (int j = 0; j < KM; ++j)
+                        if ((code[c][j] >> 8) == n) m |= 1u << (code[c][j] & 255);
+                    fwd[row] = m;
+                    if (row_token) row_token[row] = (int32_t)t;
+                }
+                node_pos[t * N + n] = row;
+            }
+        }
+    }
+}
+
+// Copies x[t] to the rows pos[t][0..per_tok) that are in [0, bound).
+template <bool kNode>
+cobalt_status launch_copy(const void* x, const int32_t* pos, int64_t T, int per_tok, int64_t d,
+                          int64_t bound, void* packed, hipStream_t s) {
+    const int64_t nch = d / 8;
+    const u32x4* xv = (const u32x4*)x;
+    u32x4* pv = (u32x4*)packed;
+    auto launch = [&](auto kernel, int64_t cg) {
+        const int64_t items = T * ((nch + 64 * cg - 1) / (64 * cg));
+        hipLaunchKernelGGL(kernel, dim3((unsigned)((items + kCopyWaves - 1) / kCopyWaves)),
+                           dim3(kCopyWaves * 64), 0, s, xv, pos, T, per_tok, nch, bound, pv);
+    };
+    if (nch >= 128)
+        per_tok == 8 ? launch(copy_kernel<2, 8, kNode>, 2) : launch(copy_kernel<2, 0, kNode>, 2);
+    else
+        per_tok == 8 ? launch(copy_kernel<1, 8, kNode>, 1) : launch(copy_kernel<1, 0, kNode>, 1);
+    COBALT_LAUNCH_CHECK();
+    return COBALT_OK;
+}
+
 }  // namespace
 
 size_t dispatch_workspace_bytes(int64_t T, int K, int G) {
-    const int64_t ntiles = (T * K + kTile - 1) / kTile;
-    return 256 + align256(sizeof(int32_t) * (size_t)G * G) +
-           align256(sizeof(uint64_t) * (size_t)std::max<int64_t>(ntiles, 1) * G);
+    return carve_bytes((T * K + kTile - 1) / kTile, G, G);
 }
+
+size_t node_dispatch_workspace_bytes(int64_t T, int N, int G) {
+    return carve_bytes((T + kNodeTile - 1) / kNodeTile, G, N);
+}
+
+namespace {
+
+template <bool kNode>
+cobalt_status launch_init(const DeviceInfo& di, int32_t* counts, int64_t ncounts,
+                          const Workspace& w, int C, hipStream_t s) {
+    const int64_t nstatus = w.ntiles * C;
+    const int64_t init_work = std::max<int64_t>(ncounts, nstatus);
+    const unsigned init_blocks = (unsigned)std::min<int64_t>(
+        std::max<int64_t>(1, (init_work + kInitThreads - 1) / kInitThreads), 4 * di.cus);
+    hipLaunchKernelGGL(init_kernel<kNode>, dim3(init_blocks), dim3(kInitThreads), 0, s, counts,
+                       ncounts, w.ctrl, w.status, nstatus);
+    COBALT_LAUNCH_CHECK();
+    return COBALT_OK;
+}
+
+template <bool kNode>
+cobalt_status launch_scan(const int32_t* counts, int R, int C, int64_t* offsets, int32_t* base,
+                          hipStream_t s) {
+    if ((int64_t)R * C <= kScanLds)
+        hipLaunchKernelGGL((scan_kernel<true, kNode>), dim3(1), dim3(kScanThreads), 0, s, counts,
+                           R, C, offsets, base);
+    else
+        hipLaunchKernelGGL((scan_kernel<false, kNode>), dim3(1), dim3(kScanThreads), 0, s, counts,
+                           R, C, offsets, base);
+    COBALT_LAUNCH_CHECK();
+    return COBALT_OK;
+}
+
+}  // namespace
 
 cobalt_status launch_dispatch(const int32_t* assigned, const int32_t* src, int64_t T, int K,
                               int G, const void* x, int64_t d, int32_t* counts, int64_t* offsets,
                               int32_t* pos, void* packed, void* ws, hipStream_t s) {
     DeviceInfo di;
     if (cobalt_status st = device_info(&di)) return st;
-    const Workspace w = carve(ws, T, K, G);
+    const Workspace w = carve(ws, (T * K + kTile - 1) / kTile, G, G);
     const int64_t TK = T * K;
     const int64_t tok_per_src = src ? 1 : std::max<int64_t>(1, T / G);
-    const int64_t nstatus = w.ntiles * G;
 
-    const int64_t init_work = std::max<int64_t>((int64_t)G * G, nstatus);
-    const unsigned init_blocks =
-        (unsigned)std::min<int64_t>(std::max<int64_t>(1, (init_work + kInitThreads - 1) / kInitThreads),
-                                    4 * di.cus);
-    hipLaunchKernelGGL(init_kernel, dim3(init_blocks), dim3(kInitThreads), 0, s, counts,
-                       (int64_t)G * G, w.ctrl, w.status, nstatus);
-    COBALT_LAUNCH_CHECK();
+    if (cobalt_status st = launch_init<false>(di, counts, (int64_t)G * G, w, G, s)) return st;
     if (T > 0) {
         const int64_t tok_per_blk =
             std::max<int64_t>(64, (T + 2 * di.cus - 1) / (2 * di.cus));
@@ -345,33 +587,51 @@ cobalt_status launch_dispatch(const int32_t* assigned, const int32_t* src, int64
                            T, K, G, tok_per_src, tok_per_blk, counts);
         COBALT_LAUNCH_CHECK();
     }
-    if ((int64_t)G * G <= kScanLds)
-        hipLaunchKernelGGL(scan_kernel<true>, dim3(1), dim3(kScanThreads), 0, s, counts, G,
-                           offsets, w.base);
-    else
-        hipLaunchKernelGGL(scan_kernel<false>, dim3(1), dim3(kScanThreads), 0, s, counts, G,
-                           offsets, w.base);
-    COBALT_LAUNCH_CHECK();
+    if (cobalt_status st = launch_scan<false>(counts, G, G, offsets, w.base, s)) return st;
     if (T == 0) return COBALT_OK;
     hipLaunchKernelGGL(rank_kernel, dim3((unsigned)w.ntiles), dim3(kRankThreads), 0, s, assigned,
                        src, K, G, tok_per_src, TK, w.ntiles, w.ctrl, w.base, w.status, pos);
     COBALT_LAUNCH_CHECK();
     if (!x) return COBALT_OK;
+    return launch_copy<false>(x, pos, T, K, d, TK, packed, s);
+}
 
-    const int64_t nch = d / 8;
-    const u32x4* xv = (const u32x4*)x;
-    u32x4* pv = (u32x4*)packed;
-    auto launch = [&](auto kernel, int64_t cg) {
-        const int64_t items = T * ((nch + 64 * cg - 1) / (64 * cg));
-        hipLaunchKernelGGL(kernel, dim3((unsigned)((items + kCopyWaves - 1) / kCopyWaves)),
-                           dim3(kCopyWaves * 64), 0, s, xv, pos, T, K, nch, TK, pv);
-    };
-    if (nch >= 128)
-        K == 8 ? launch(copy_kernel<2, 8>, 2) : launch(copy_kernel<2, 0>, 2);
+cobalt_status launch_node_dispatch(const int32_t* assigned, const int32_t* src, int64_t T, int K,
+                                   int N, int g, const void* x, int64_t d, int32_t* counts,
+                                   int64_t* offsets, int32_t* node_pos, uint32_t* fwd,
+                                   int32_t* row_token, void* packed, void* ws, hipStream_t s) {
+    DeviceInfo di;
+    if (cobalt_status st = device_info(&di)) return st;
+    const int G = N * g;
+    const Workspace w = carve(ws, (T + kNodeTile - 1) / kNodeTile, G, N);
+    const int64_t tok_per_src = src ? 1 : std::max<int64_t>(1, T / G);
+
+    if (cobalt_status st = launch_init<true>(di, counts, (int64_t)G * N, w, N, s)) return st;
+    if (T > 0) {
+        const int64_t tok_per_blk =
+            std::max<int64_t>(kCountThreads, (T + 2 * di.cus - 1) / (2 * di.cus));
+        const unsigned cblocks = (unsigned)((T + tok_per_blk - 1) / tok_per_blk);
+        if (K == 8)
+            hipLaunchKernelGGL(node_count_kernel<8>, dim3(cblocks), dim3(kCountThreads), 0, s,
+                               assigned, src, T, K, N, g, tok_per_src, tok_per_blk, counts);
+        else
+            hipLaunchKernelGGL(node_count_kernel<0>, dim3(cblocks), dim3(kCountThreads), 0, s,
+                               assigned, src, T, K, N, g, tok_per_src, tok_per_blk, counts);
+        COBALT_LAUNCH_CHECK();
+    }
+    if (cobalt_status st = launch_scan<true>(counts, G, N, offsets, w.base, s)) return st;
+    if (T == 0) return COBALT_OK;
+    if (K == 8)
+        hipLaunchKernelGGL(node_rank_kernel<8>, dim3((unsigned)w.ntiles), dim3(kRankThreads), 0,
+                           s, assigned, src, T, K, N, g, tok_per_src, w.ntiles, w.ctrl, w.base,
+                           w.status, node_pos, fwd, row_token);
     else
-        K == 8 ? launch(copy_kernel<1, 8>, 1) : launch(copy_kernel<1, 0>, 1);
+        hipLaunchKernelGGL(node_rank_kernel<0>, dim3((unsigned)w.ntiles), dim3(kRankThreads), 0,
+                           s, assigned, src, T, K, N, g, tok_per_src, w.ntiles, w.ctrl, w.base,
+                           w.status, node_pos, fwd, row_token);
     COBALT_LAUNCH_CHECK();
-    return COBALT_OK;
+    if (!x) return COBALT_OK;
+    return launch_copy<true>(x, node_pos, T, N, d, T * std::min(K, N), packed, s);
 }
 
 }  // namespace cobalt

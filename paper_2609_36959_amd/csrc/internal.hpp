@@ -51,6 +51,11 @@ cobalt_status launch_dispatch(const int32_t* assigned, const int32_t* src, int64
                               int G, const void* x, int64_t d, int32_t* counts,
                               int64_t* offsets, int32_t* pos, void* packed, void* ws,
                               hipStream_t s);
+size_t node_dispatch_workspace_bytes(int64_t T, int N, int G);
+cobalt_status launch_node_dispatch(const int32_t* assigned, const int32_t* src, int64_t T, int K,
+                                   int N, int g, const void* x, int64_t d, int32_t* counts,
+                                   int64_t* offsets, int32_t* node_pos, uint32_t* fwd,
+                                   int32_t* row_token, void* packed, void* ws, hipStream_t s);
 cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* gates, int64_t T,
                              int K, int64_t d, void* y, float* y32, hipStream_t s);
 size_t replica_load_workspace_bytes(int64_t T, int K, int E, int G);

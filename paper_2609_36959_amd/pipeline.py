@@ -90,6 +90,25 @@ class RoutingStep:
         B.cobalt_replica_load(self.topk, self.assigned, self.w.E, self.w.G, self.replica_load,
                               self.load_workspace, stream=stream)
 
+    def node_pack(self, stream=None):
+        """Node-deduplicated dispatch layout and pack of the current
+        assignment (one row per (token, destination node)); buffers are
+        allocated on first use."""
+        w = self.w
+        if getattr(self, "node_packed", None) is None:
+            dev, cap = self.device, w.T * min(w.K, w.N)
+            self.node_counts = torch.empty(w.G, w.N, dtype=torch.int32, device=dev)
+            self.node_offsets = torch.empty(w.G * w.N + 1, dtype=torch.int64, device=dev)
+            self.node_pos = torch.empty(w.T, w.N, dtype=torch.int32, device=dev)
+            self.fwd_mask = torch.empty(cap, dtype=torch.int32, device=dev)
+            self.row_token = torch.empty(cap, dtype=torch.int32, device=dev)
+            self.node_packed = torch.empty(cap, w.d, dtype=torch.bfloat16, device=dev)
+            self.node_workspace = B.node_workspace_for(w.T, w.N, w.g, device=dev)
+        B.cobalt_node_dispatch_pack(self.assigned, self.src, w.N, w.g, self.x, self.node_counts,
+                                    self.node_offsets, self.node_pos, self.fwd_mask,
+                                    self.row_token, self.node_packed, self.node_workspace,
+                                    stream=stream)
+
     def run(self, mode=0, stream=None):
         self.stats(stream)
         self.assign(mode, stream)

@@ -58,6 +58,12 @@ def test_workspace_size_query():
     assert L.cobalt_dispatch_workspace_bytes(-1, 8, 64) == 0
     assert L.cobalt_dispatch_workspace_bytes(10, 17, 64) == 0
     assert L.cobalt_dispatch_workspace_bytes(10, 8, 513) == 0
+    n1 = L.cobalt_node_dispatch_workspace_bytes(131072, 8, 8)
+    n2 = L.cobalt_node_dispatch_workspace_bytes(4096, 2, 4)
+    assert n1 > n2 > 0 and n1 % 256 == 0
+    assert L.cobalt_node_dispatch_workspace_bytes(10, 17, 1) == 0
+    assert L.cobalt_node_dispatch_workspace_bytes(10, 2, 33) == 0
+    assert L.cobalt_node_dispatch_workspace_bytes(-1, 2, 4) == 0
 
 
 def _p(v):
@@ -92,6 +98,23 @@ def test_argument_checks_reject_before_device_work():
                                   None) == EINVAL  # workspace too small
     assert L.cobalt_dispatch_pack(fake, None, 9, 2, 4, None, 0, fake, fake, fake, None, fake,
                                   1 << 20, None) == EINVAL  # T % G != 0 without src_rank
+    # node dispatch: x without packed, null forwarding index, N or g out of
+    # range, misaligned or short workspace, T % G != 0 without src_rank
+    nargs = [fake, None, 8, 2, 2, 2]
+    assert L.cobalt_node_dispatch_pack(*nargs, fake, 8, fake, fake, fake, fake, None, None, fake,
+                                       1 << 20, None) == EINVAL
+    assert L.cobalt_node_dispatch_pack(*nargs, None, 0, fake, fake, fake, None, None, None, fake,
+                                       1 << 20, None) == EINVAL
+    assert L.cobalt_node_dispatch_pack(fake, None, 8, 2, 17, 1, None, 0, fake, fake, fake, fake,
+                                       None, None, fake, 1 << 20, None) == EINVAL
+    assert L.cobalt_node_dispatch_pack(fake, None, 8, 2, 2, 33, None, 0, fake, fake, fake, fake,
+                                       None, None, fake, 1 << 20, None) == EINVAL
+    assert L.cobalt_node_dispatch_pack(*nargs, None, 0, fake, fake, fake, fake, None, None,
+                                       _p(4100), 1 << 20, None) == EINVAL
+    assert L.cobalt_node_dispatch_pack(*nargs, None, 0, fake, fake, fake, fake, None, None, fake,
+                                       16, None) == EINVAL
+    assert L.cobalt_node_dispatch_pack(fake, None, 9, 2, 2, 2, None, 0, fake, fake, fake, fake,
+                                       None, None, fake, 1 << 20, None) == EINVAL
     # combine: d not a multiple of 8, misaligned rows
     assert L.cobalt_combine(fake, fake, fake, 8, 2, 12, fake, None, None) == EINVAL
     assert L.cobalt_combine(_p(4098), fake, fake, 8, 2, 16, fake, None, None) == EINVAL
