@@ -61,10 +61,13 @@ def lib():
         L.ref_node_dispatch.argtypes = [P, P, i64, i32, i32, i32, P, i64, P, P, P, P, P, P]
         L.ref_combine.argtypes = [P, i64, P, P, i64, i32, i64, P, P]
         L.ref_traffic.argtypes = [P, P, i64, i32, i32, i32, P, P, P]
+        L.ref_count_ema.argtypes = [P, i64, ctypes.c_float, i32, i32, P]
+        L.ref_ochiai.argtypes = [P, P, i32, P]
         L.ref_replica_load.argtypes = [P, P, i64, i32, i32, i32, P]
         L.ref_intra_node_rebalance.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P]
         for f in ("ref_coact_stats", "ref_layout_tables", "ref_assign", "ref_dispatch",
-                  "ref_node_dispatch", "ref_combine", "ref_traffic", "ref_replica_load", "ref_intra_node_rebalance"):
+                  "ref_node_dispatch", "ref_combine", "ref_traffic", "ref_count_ema", "ref_ochiai",
+                  "ref_replica_load", "ref_intra_node_rebalance"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -227,6 +230,29 @@ def traffic(assigned, N, g, src=None):
     _check(lib().ref_traffic(_p(assigned), _p(src), T, K, N, g, ctypes.byref(V),
                              ctypes.byref(cp), _p(load)), "traffic")
     return V.value, cp.value, load
+
+
+def count_ema(counts, decay, ema=None, init=False, clear=False):
+    """One EMA update (fp32) of ema from uint32 counts of any shape; returns
+    (ema, counts), counts zeroed if clear. ema is updated in place if given."""
+    counts = np.array(counts, dtype=np.uint32, copy=True) if not clear else counts
+    assert counts.dtype == np.uint32 and counts.flags.c_contiguous
+    ema = np.zeros(counts.shape, np.float32) if ema is None else ema
+    assert ema.dtype == np.float32 and ema.flags.c_contiguous and ema.shape == counts.shape
+    _check(lib().ref_count_ema(_p(counts), counts.size, float(decay), int(init), int(clear),
+                               _p(ema)), "count_ema")
+    return ema, counts
+
+
+def ochiai(coact, count):
+    """Ochiai similarity [E, E] fp32 from co-activation and expert counts."""
+    coact = _c(coact, np.uint32)
+    count = _c(count, np.uint32)
+    E = count.size
+    assert coact.shape == (E, E)
+    out = np.zeros((E, E), np.float32)
+    _check(lib().ref_ochiai(_p(coact), _p(count), E, _p(out)), "ochiai")
+    return out
 
 
 def replica_load(topk, assigned, E, G, load=None):

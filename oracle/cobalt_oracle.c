@@ -482,6 +482,54 @@ int ref_traffic(const int32_t* assigned, const int32_t* src, int64_t T, int32_t 
 }
 
 /* ---------------------------------------------------------------------- */
+/* Exponential moving averages of the planner's statistics (Section 3.2:  */
+/* Stage 1 keeps EMAs of w_e, the tasks of expert e, and of c_ij, the      */
+/* tokens selecting both i and j; Stage 2 keeps an EMA of each replica's   */
+/* tasks). The decay is not given in the paper; it is a parameter here.    */
+/* One update of an EMA m with this step's count x, in fp32:              */
+/*   init:      m = x                                                      */
+/*   otherwise: m = fma(decay, m, (1 - decay) * x)                         */
+/* where x is the count converted to fp32 and 1 - decay is rounded to      */
+/* fp32 once. clear: the counts are set to 0 after they are read.          */
+/* ---------------------------------------------------------------------- */
+int ref_count_ema(uint32_t* counts, int64_t n, float decay, int32_t init, int32_t clear,
+                  float* ema)
+{
+    if (n < 0 || !(decay >= 0.0f && decay <= 1.0f)) return REF_EINVAL;
+    float gain = 1.0f - decay;
+    for (int64_t i = 0; i < n; ++i) {
+        float x = (float)counts[i];
+        if (init) ema[i] = x;
+        else ema[i] = fmaf(decay, ema[i], gain * x);
+        if (clear) counts[i] = 0;
+    }
+    return REF_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Ochiai similarity of experts i and j (Section 1, footnote on Fig. 3):  */
+/* with A_i the set of tokens that select expert i,                        */
+/*   O_ij = |A_i & A_j| / sqrt(|A_i| |A_j|),                               */
+/* from the co-activation counts: |A_i & A_j| = coact[i][j] for i != j and */
+/* |A_i| = count[i]. O_ii = 1 for an expert some token selects. A pair     */
+/* with no common token, or an expert no token selects, gives 0. In fp32: */
+/*   O_ij = (float)c / sqrtf((float)n_i * (float)n_j).                     */
+/* ---------------------------------------------------------------------- */
+int ref_ochiai(const uint32_t* coact, const uint32_t* count, int32_t E, float* ochiai)
+{
+    if (E < 1) return REF_EINVAL;
+    for (int32_t i = 0; i < E; ++i)
+        for (int32_t j = 0; j < E; ++j) {
+            uint32_t c = i == j ? count[i] : coact[(int64_t)i * E + j];
+            float o = 0.0f;
+            if (c != 0 && count[i] != 0 && count[j] != 0)
+                o = (float)c / sqrtf((float)count[i] * (float)count[j]);
+            ochiai[(int64_t)i * E + j] = o;
+        }
+    return REF_OK;
+}
+
+/* ---------------------------------------------------------------------- */
 /* Per-replica workload (Section 3.1: w_er, the tasks of expert e executed */
 /* by its replica on rank r). load [E][G] += counts; pairs with an id or   */
 /* rank out of range are skipped.                                          */
