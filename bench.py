@@ -354,6 +354,34 @@ def main():
         "hbm_frac": nb / (node_ms * 1e-3) / HBM_PEAK,
         "traffic": measured_traffic("cobalt_node_dispatch_pack", wl_name),
         "pair_pack_ms": call_ms["cobalt_dispatch_pack"], "node_pack_ms": node_ms}
+    # planner statistics of one step: EMA update of the co-activation and
+    # expert counts, and the Ochiai similarity (the Fig. 3 statistic)
+    st.coact.zero_()
+    st.count.zero_()
+    with torch.cuda.stream(stream):
+        st.stats(stream=stream)
+        st.ema(0.9, B.EMA_INIT, stream=stream)
+        ev[0].record(stream)
+        for _ in range(args.steps):
+            st.ema(0.9, 0, stream=stream)
+        ev[1].record(stream)
+    torch.cuda.synchronize()
+    result["extra_calls_ms"]["cobalt_coact_ema"] = ev[0].elapsed_time(ev[1]) / args.steps
+    pairs = torch.triu(st.coact != 0, diagonal=1)
+    result["planner_statistics"] = {
+        "ochiai_mean_coactivated_pairs": float(st.ochiai[pairs].mean().item()),
+        "coactivated_pairs": int(pairs.sum().item()),
+        "pairs": w.E * (w.E - 1) // 2}
+    cl = W.clusters(w, seed)
+    if cl is not None:
+        same = torch.zeros(w.E, w.E, dtype=torch.bool, device="cuda")
+        idx = torch.from_numpy(cl).cuda()
+        same[idx[:, :, None], idx[:, None, :]] = True
+        inside = pairs & same
+        result["planner_statistics"]["ochiai_mean_planted_cluster_pairs"] = \
+            float(st.ochiai[inside].mean().item())
+        result["planner_statistics"]["ochiai_mean_other_pairs"] = \
+            float(st.ochiai[pairs & ~same].mean().item())
     result["routing"] = routing_quality(st, torch, B, W)
     result["routing"]["stage2_rebalance"] = stage2_demo(st, torch, B, W)
     if not args.no_cpu_baseline:

@@ -261,6 +261,43 @@ cobalt_status cobalt_intra_node_rebalance(int32_t N, int32_t gpus_per_node, int3
                                           int32_t* host_new_owner_rank, float* host_rank_load);
 
 /* ------------------------------------------------------------------------
+ * Planner statistics (Section 3.2): exponential moving averages of the
+ * step's counts, and the Ochiai similarity of expert pairs (Section 1, the
+ * footnote on Fig. 3). The paper gives no decay; it is a parameter.
+ *
+ * One EMA update of m with a count x, in fp32:
+ *   COBALT_EMA_INIT set:  m = x
+ *   otherwise:            m = fma(decay, m, (1 - decay) * x)
+ * with x the count rounded to fp32 and 1 - decay rounded to fp32 once.
+ * COBALT_EMA_CLEAR set: the counts are set to 0 after they are read, so the
+ * next step's statistics start from zero with no separate clearing call.
+ * decay must lie in [0, 1]; flags other than these two bits are rejected.
+ * ---------------------------------------------------------------------- */
+#define COBALT_EMA_INIT 1
+#define COBALT_EMA_CLEAR 2
+
+/* Stage 1's statistics: EMAs of c_ij and w_e from the counts of
+ * cobalt_coact_stats, and the Ochiai similarity of the step's counts.
+ * coact [E][E] uint32 in (cleared with COBALT_EMA_CLEAR); expert_count [E]
+ * uint32 in (cleared likewise).
+ * ema_coact [E][E] fp32 in/out (may be NULL); ema_count [E] fp32 in/out (may
+ * be NULL); ochiai [E][E] fp32 out (may be NULL):
+ *   ochiai[i][j] = coact[i][j] / sqrt(expert_count[i] * expert_count[j]),
+ *   ochiai[i][i] = 1 for an expert with a nonzero count,
+ * and 0 where the pair shares no token or either count is 0, each
+ * operation one correctly rounded fp32 operation. */
+cobalt_status cobalt_coact_ema(uint32_t* coact, uint32_t* expert_count, int32_t E, float decay,
+                               int32_t flags, float* ema_coact, float* ema_count, float* ochiai,
+                               void* stream);
+
+/* EMA of any n uint32 counts, e.g. Stage 2's replica-level w_er from
+ * cobalt_replica_load (initialised by the caller, e.g. from the planned
+ * workload division, before the first update). counts [n] uint32 in (cleared
+ * with COBALT_EMA_CLEAR); ema [n] fp32 in/out (may be NULL to clear only). */
+cobalt_status cobalt_count_ema(uint32_t* counts, int64_t n, float decay, int32_t flags,
+                               float* ema, void* stream);
+
+/* ------------------------------------------------------------------------
  * Debug check of routing inputs (synchronous; allocates a few bytes).
  * Checks 0 <= topk_idx < E, distinct experts within each token, and, if
  * src_rank is given, 0 <= src_rank < G and non-decreasing. Returns COBALT_OK

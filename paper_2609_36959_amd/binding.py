@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
         "cobalt_node_dispatch_pack": ([P, P, i64, i32, i32, i32, P, i64, P, P, P, P, P, P, P, sz,
                                        P], ctypes.c_int),
         "cobalt_combine": ([P, P, P, i64, i32, i64, P, P, P], ctypes.c_int),
+        "cobalt_coact_ema": ([P, P, i32, ctypes.c_float, i32, P, P, P, P], ctypes.c_int),
+        "cobalt_count_ema": ([P, i64, ctypes.c_float, i32, P, P], ctypes.c_int),
         "cobalt_validate_routing": ([P, P, i64, i32, i32, i32, P, P], ctypes.c_int),
         "cobalt_replica_load_workspace_bytes": ([i64, i32, i32, i32], sz),
         "cobalt_replica_load": ([P, P, i64, i32, i32, i32, P, P, sz, P], ctypes.c_int),
@@ -228,6 +230,27 @@ def cobalt_node_dispatch_pack(assigned_rank: torch.Tensor, src_rank: Optional[to
           _dev(packed, "packed", BF16, None if packed is None else (cap, d)),
           _dev(workspace, "workspace", WS),
           workspace.numel() * workspace.element_size(), _stream(stream))
+
+
+EMA_INIT, EMA_CLEAR = 1, 2
+
+
+def cobalt_coact_ema(coact: torch.Tensor, expert_count: torch.Tensor, decay: float,
+                     flags: int = 0, ema_coact: Optional[torch.Tensor] = None,
+                     ema_count: Optional[torch.Tensor] = None,
+                     ochiai: Optional[torch.Tensor] = None, stream=None) -> None:
+    E = expert_count.shape[0]
+    _call("cobalt_coact_ema", _dev(coact, "coact", U32, (E, E)),
+          _dev(expert_count, "expert_count", U32, (E,)), E, float(decay), int(flags),
+          _dev(ema_coact, "ema_coact", F32, (E, E)), _dev(ema_count, "ema_count", F32, (E,)),
+          _dev(ochiai, "ochiai", F32, (E, E)), _stream(stream))
+
+
+def cobalt_count_ema(counts: torch.Tensor, decay: float, flags: int = 0,
+                     ema: Optional[torch.Tensor] = None, stream=None) -> None:
+    n = counts.numel()
+    _call("cobalt_count_ema", _dev(counts, "counts", U32), n, float(decay), int(flags),
+          _dev(ema, "ema", F32, tuple(counts.shape)), _stream(stream))
 
 
 def cobalt_combine(expert_out: torch.Tensor, pos: torch.Tensor, gates: torch.Tensor,

@@ -246,6 +246,30 @@ extern "C" cobalt_status cobalt_node_dispatch_pack(const int32_t* assigned, cons
                                 node_pos, fwd, row_token, packed, ws, (hipStream_t)stream);
 }
 
+namespace {
+bool ema_args_ok(float decay, int32_t flags) {
+    return decay >= 0.0f && decay <= 1.0f && (flags & ~(COBALT_EMA_INIT | COBALT_EMA_CLEAR)) == 0;
+}
+}  // namespace
+
+extern "C" cobalt_status cobalt_coact_ema(uint32_t* coact, uint32_t* count, int32_t E,
+                                          float decay, int32_t flags, float* ema_coact,
+                                          float* ema_count, float* ochiai, void* stream) {
+    if (E < 1 || E > kMaxE || !coact || !count || !ema_args_ok(decay, flags))
+        return COBALT_EINVAL;
+    return launch_coact_ema(coact, count, E, decay, flags & COBALT_EMA_INIT,
+                            flags & COBALT_EMA_CLEAR, ema_coact, ema_count, ochiai,
+                            (hipStream_t)stream);
+}
+
+extern "C" cobalt_status cobalt_count_ema(uint32_t* counts, int64_t n, float decay,
+                                          int32_t flags, float* ema, void* stream) {
+    if (n < 0 || !ema_args_ok(decay, flags)) return COBALT_EINVAL;
+    if (n > 0 && !counts) return COBALT_EINVAL;
+    return launch_count_ema(counts, n, decay, flags & COBALT_EMA_INIT, flags & COBALT_EMA_CLEAR,
+                            ema, (hipStream_t)stream);
+}
+
 extern "C" cobalt_status cobalt_combine(const void* eo, const int32_t* pos, const float* gates,
                                         int64_t T, int32_t K, int64_t d, void* y, float* y32,
                                         void* stream) {

@@ -62,6 +62,11 @@ size_t replica_load_workspace_bytes(int64_t T, int K, int E, int G);
 cobalt_status launch_replica_load(const int32_t* topk, const int32_t* assigned, int64_t T, int K,
                                   int E, int G, uint32_t* load, void* ws, size_t ws_bytes,
                                   hipStream_t s);
+cobalt_status launch_count_ema(uint32_t* counts, int64_t n, float decay, bool init, bool clear,
+                               float* ema, hipStream_t s);
+cobalt_status launch_coact_ema(uint32_t* coact, uint32_t* count, int E, float decay, bool init,
+                               bool clear, float* ema_coact, float* ema_count, float* ochiai,
+                               hipStream_t s);
 cobalt_status launch_validate(const int32_t* topk, const int32_t* src, int64_t T, int K, int E,
                               int G, uint32_t* dflags, hipStream_t s);
 

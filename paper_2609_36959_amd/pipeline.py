@@ -109,6 +109,18 @@ class RoutingStep:
                                     self.row_token, self.node_packed, self.node_workspace,
                                     stream=stream)
 
+    def ema(self, decay: float, flags: int = 0, stream=None):
+        """Folds the accumulated counts into the planner EMAs (ema_coact,
+        ema_count) and writes the Ochiai similarity of the counts; buffers are
+        allocated on first use. flags: B.EMA_INIT, B.EMA_CLEAR."""
+        if getattr(self, "ochiai", None) is None:
+            E, dev = self.w.E, self.device
+            self.ema_coact = torch.zeros(E, E, dtype=torch.float32, device=dev)
+            self.ema_count = torch.zeros(E, dtype=torch.float32, device=dev)
+            self.ochiai = torch.zeros(E, E, dtype=torch.float32, device=dev)
+        B.cobalt_coact_ema(self.coact, self.count, decay, flags, self.ema_coact, self.ema_count,
+                           self.ochiai, stream=stream)
+
     def run(self, mode=0, stream=None):
         self.stats(stream)
         self.assign(mode, stream)

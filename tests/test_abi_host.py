@@ -115,6 +115,18 @@ def test_argument_checks_reject_before_device_work():
                                        16, None) == EINVAL
     assert L.cobalt_node_dispatch_pack(fake, None, 9, 2, 2, 2, None, 0, fake, fake, fake, fake,
                                        None, None, fake, 1 << 20, None) == EINVAL
+    # EMA: decay outside [0, 1] or NaN, unknown flags, null counts, E out of range
+    f = ctypes.c_float
+    assert L.cobalt_coact_ema(fake, fake, 8, f(1.5), 0, fake, None, None, None) == EINVAL
+    assert L.cobalt_coact_ema(fake, fake, 8, f(float("nan")), 0, fake, None, None,
+                              None) == EINVAL
+    assert L.cobalt_coact_ema(fake, fake, 8, f(0.5), 4, fake, None, None, None) == EINVAL
+    assert L.cobalt_coact_ema(None, fake, 8, f(0.5), 0, fake, None, None, None) == EINVAL
+    assert L.cobalt_coact_ema(fake, fake, 4097, f(0.5), 0, fake, None, None, None) == EINVAL
+    assert L.cobalt_count_ema(fake, 10, f(-0.5), 0, fake, None) == EINVAL
+    assert L.cobalt_count_ema(None, 10, f(0.5), 0, fake, None) == EINVAL
+    assert L.cobalt_count_ema(fake, -1, f(0.5), 0, fake, None) == EINVAL
+    assert L.cobalt_count_ema(None, 0, f(0.5), 2, None, None) == 0  # nothing to do
     # combine: d not a multiple of 8, misaligned rows
     assert L.cobalt_combine(fake, fake, fake, 8, 2, 12, fake, None, None) == EINVAL
     assert L.cobalt_combine(_p(4098), fake, fake, 8, 2, 16, fake, None, None) == EINVAL
