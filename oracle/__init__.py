@@ -63,11 +63,12 @@ def lib():
         L.ref_traffic.argtypes = [P, P, i64, i32, i32, i32, P, P, P]
         L.ref_count_ema.argtypes = [P, i64, ctypes.c_float, i32, i32, P]
         L.ref_ochiai.argtypes = [P, P, i32, P]
+        L.ref_plan_layout.argtypes = [i32, i32, i32, i32, P, P, ctypes.c_float, P, P, P, P, P]
         L.ref_replica_load.argtypes = [P, P, i64, i32, i32, i32, P]
         L.ref_intra_node_rebalance.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P]
         for f in ("ref_coact_stats", "ref_layout_tables", "ref_assign", "ref_dispatch",
                   "ref_node_dispatch", "ref_combine", "ref_traffic", "ref_count_ema", "ref_ochiai",
-                  "ref_replica_load", "ref_intra_node_rebalance"):
+                  "ref_replica_load", "ref_intra_node_rebalance", "ref_plan_layout"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -279,3 +280,20 @@ def intra_node_rebalance(N, g, E, slot_table, owner, replica_load):
     _check(lib().ref_intra_node_rebalance(N, g, E, S, _p(st), _p(own), _p(rl), _p(out),
                                           _p(new_own), _p(rank_load)), "intra_node_rebalance")
     return out, new_own, rank_load
+
+
+def plan_layout(N, g, E, S, coact_ema, count_ema, eps):
+    """Stage-1 greedy planner. Returns (slot_table [G, S] i32, owner [E] i32,
+    plan [E, G] f32, objective float, feasible bool)."""
+    G = N * g
+    c = _c(coact_ema, np.float32)
+    w = _c(count_ema, np.float32)
+    assert c.shape == (E, E) and w.shape == (E,)
+    table = np.zeros((G, S), np.int32)
+    owner = np.zeros(E, np.int32)
+    plan = np.zeros((E, G), np.float32)
+    obj = ctypes.c_double()
+    feas = ctypes.c_int32()
+    _check(lib().ref_plan_layout(N, g, E, S, _p(c), _p(w), float(eps), _p(table), _p(owner),
+                                 _p(plan), ctypes.byref(obj), ctypes.byref(feas)), "plan_layout")
+    return table, owner, plan, obj.value, bool(feas.value)

@@ -653,3 +653,594 @@ done:
     free(node_mask); free(rank_mask); free(owner); free(reps); free(dest); free(load); free(used);
     return rc;
 }
+
+/* ---------------------------------------------------------------------- */
+/* Periodic global planning (Section 3.2, Stage 1; Eq. 3 and its MILP in   */
+/* the appendix). The paper solves Eq. 3 exactly with a MILP solver; this  */
+/* is a greedy heuristic for the same objective and constraints, stated    */
+/* step by step below, and this oracle follows those steps literally.      */
+/*                                                                        */
+/* Objective: sum over nodes n and pairs i < j of c_ij [i, j both on n].   */
+/* Constraints: every expert on some rank; at most S replicas per rank; no */
+/* expert twice on a rank; planned work l_er >= 0 only where e is held,    */
+/* sum_r l_er = w_e; sum_e l_er <= cap = (1 + eps) W / G per rank, where   */
+/* W = sum_e w_e. Pair weights are quantised to q_ij = llrint(256 c_ij) in */
+/* int64 so that every gain is an exact integer sum.                       */
+/*                                                                        */
+/* gain(e, n) = sum of q_ex over experts x != e already on node n.         */
+/* need(x)    = 1 if x <= cap, else ceil(x / cap): ranks a share x needs.  */
+/*                                                                        */
+/* 1. Work placement. Experts in decreasing w (ties: smaller id). Each    */
+/*    takes nodes one at a time until its work is placed: among nodes not */
+/*    holding it with a free slot, the best by (the whole remainder fits  */
+/*    in the node's spare work g cap - work and its free slots, some      */
+/*    spare work left, spare work, gain), ties to the smaller node. A     */
+/*    fitting node takes the remainder; otherwise the node takes what its */
+/*    spare work and free slots allow (if nothing, the remainder). The    */
+/*    share reserves need(share) slots of the node, at most its free      */
+/*    slots and g. If every node was tried, the rest goes to the last one.*/
+/*    Steps 1 and 1b use g S - R slots per node, R = min(g, (G S - sum_e  */
+/*    need(w_e)) / N) (integer division, 0 if negative): the free slots   */
+/*    the repair of step 2 may split work into. Step 1 picks among nodes  */
+/*    within g S - R slots first, and uses all g S slots when that finds  */
+/*    no node at all, or only non-fitting ones while a node fits with    */
+/*    all slots.                                                          */
+/*    Local search: an expert placed whole on one node in one slot is     */
+/*    single. Sweeps over single experts a in increasing id apply, for    */
+/*    each a, the best of (ties: moves before swaps, then smaller node or */
+/*    smaller b)                                                          */
+/*      move a to node m with a free slot:                                */
+/*        delta = gain(a, m) - gain(a, n_a)                               */
+/*      swap a with a single b on another node:                           */
+/*        delta = gain(a, n_b) - gain(a, n_a) + gain(b, n_a)              */
+/*                - gain(b, n_b) - 2 q_ab                                 */
+/*    if its delta is positive and every node it changes ends with work   */
+/*    at most g cap or no more than before. Sweeps repeat until one       */
+/*    changes nothing (at most 64 sweeps).                                */
+/* 2. Ranks, node by node. Each share is cut into need(share) equal      */
+/*    pieces; pieces in decreasing work (ties: smaller e, earlier piece)  */
+/*    go to the rank of the node with least planned work (ties: fewer     */
+/*    replicas, smaller rank) that holds fewer than min(S, ceil(pieces /  */
+/*    g)) replicas, so that free slots stay spread over the ranks,        */
+/*    and does not hold the expert. If some piece finds none, the node is */
+/*    laid out round-robin instead: experts by decreasing piece count     */
+/*    (ties: smaller e), the                                              */
+/*    node's p-th piece on rank p mod g.                                  */
+/*    Repair, an augmenting-path step on the flow network expert -> rank: */
+/*    while the most loaded rank h of the node (ties: smaller) exceeds    */
+/*    cap, search breadth-first from h: from rank a, for each expert e    */
+/*    with work on a (increasing e), each unvisited rank b of the node    */
+/*    (increasing) that holds e, or has a free slot, is reached through   */
+/*    e. The first reached rank t below cap ends the search; the work     */
+/*    min(load_h - cap, cap - load_t, the work of each path expert on its */
+/*    rank) moves along the path, adding replicas where b did not hold e. */
+/*    If no such rank is reachable and h has a free slot, a slot swap:    */
+/*    eh is the expert with the most work on h (ties: smaller e); among   */
+/*    the under-cap ranks u with no free slot and without eh, the least   */
+/*    loaded (ties: smaller) that holds an expert x with less work than   */
+/*    eh has on h and not held by h, x the one with least work (ties:     */
+/*    smaller). x moves whole from u to h, then m = min(load_h - cap +    */
+/*    w_x, cap - load_u + w_x, l_eh,h) of eh moves to a new replica on u, */
+/*    if m > w_x. Stop when neither applies or a path move is below       */
+/*    cap 1e-12 (at most 4 g^2 S moves).                                  */
+/* 3. Co-activation replicas. While some (e, n) with e not on n, a free   */
+/*    slot on n and positive gain exists: add the one with the largest    */
+/*    gain (ties: larger w, smaller e, smaller n) on the rank of n with   */
+/*    fewest replicas (ties: smaller), with no planned work.              */
+/* owner[e]: the rank with the most planned work for e (ties: smaller).   */
+/* plan [E][G]: planned work l_er (fp32 of the double sums); objective:    */
+/* the quantised objective / 256; feasible: every rank's planned work is   */
+/* at most cap (1 + 1e-9).                                                */
+/* ---------------------------------------------------------------------- */
+static int64_t plan_q(const int64_t* q, int32_t E, int32_t a, int32_t b)
+{
+    if (a == b) return 0;
+    return a < b ? q[(int64_t)a * E + b] : q[(int64_t)b * E + a];
+}
+
+static int64_t plan_gain(const int64_t* q, const uint8_t* on, int32_t E, int32_t N, int32_t e,
+                         int32_t n)
+{
+    int64_t s = 0;
+    for (int32_t x = 0; x < E; ++x)
+        if (x != e && on[(int64_t)x * N + n]) s += plan_q(q, E, e, x);
+    return s;
+}
+
+static int64_t plan_need(double x, double cap)
+{
+    if (x <= cap) return 1;
+    return (int64_t)ceil(x / cap);
+}
+
+struct plan_piece { double load; int32_t e, c; };
+
+static int piece_before(const struct plan_piece* a, const struct plan_piece* b)
+{
+    if (a->load != b->load) return a->load > b->load;
+    if (a->e != b->e) return a->e < b->e;
+    return a->c < b->c;
+}
+
+/* replicas on rank r: slots in use */
+static int32_t plan_used(const int32_t* slot_table, int32_t S, int32_t r)
+{
+    int32_t k = 0;
+    while (k < S && slot_table[(int64_t)r * S + k] >= 0) ++k;
+    return k;
+}
+
+static int plan_holds(const int32_t* slot_table, int32_t S, int32_t r, int32_t e)
+{
+    for (int32_t k = 0; k < S; ++k)
+        if (slot_table[(int64_t)r * S + k] == e) return 1;
+    return 0;
+}
+
+static double plan_rank_load(const double* pl, int32_t E, int32_t G, int32_t r)
+{
+    double l = 0.0;
+    for (int32_t e = 0; e < E; ++e) l += pl[(int64_t)e * G + r];
+    return l;
+}
+
+int ref_plan_layout(int32_t N, int32_t g, int32_t E, int32_t S, const float* coact_ema,
+                    const float* count_ema, float eps, int32_t* slot_table, int32_t* owner,
+                    float* plan, double* objective, int32_t* feasible)
+{
+    if (N < 1 || N > 16 || g < 1 || g > 32 || E < 1 || S < 1) return REF_EINVAL;
+    if (!(eps >= 0.0f) || isinf(eps)) return REF_EINVAL;
+    int32_t G = N * g;
+    if ((int64_t)G * S < E) return REF_EINVAL;
+    for (int32_t e = 0; e < E; ++e)
+        if (!(count_ema[e] >= 0.0f) || isinf(count_ema[e])) return REF_EDATA;
+    for (int32_t i = 0; i < E; ++i)
+        for (int32_t j = i + 1; j < E; ++j) {
+            float c = coact_ema[(int64_t)i * E + j];
+            if (!(c >= 0.0f) || !(c <= 1099511627776.0f)) return REF_EDATA; /* 2^40 */
+        }
+
+    int rc = REF_OK;
+    int64_t* q = (int64_t*)calloc((size_t)E * E, sizeof(int64_t));
+    uint8_t* on = (uint8_t*)calloc((size_t)E * N, 1);
+    double* share = (double*)calloc((size_t)E * N, sizeof(double));
+    int64_t* pieces = (int64_t*)calloc((size_t)E * N, sizeof(int64_t));
+    int32_t* order = (int32_t*)malloc((size_t)E * sizeof(int32_t));
+    int64_t* used = (int64_t*)calloc((size_t)N, sizeof(int64_t));
+    double* work = (double*)calloc((size_t)N, sizeof(double));
+    double* pl = (double*)calloc((size_t)E * G, sizeof(double));
+    struct plan_piece* items = (struct plan_piece*)malloc((size_t)g * S * sizeof(struct plan_piece));
+    double* rload = (double*)calloc((size_t)g, sizeof(double));
+    int32_t* dest = (int32_t*)malloc((size_t)g * S * sizeof(int32_t));
+    if (!q || !on || !share || !pieces || !order || !used || !work || !pl || !items || !rload ||
+        !dest) {
+        rc = REF_EINVAL;
+        goto done;
+    }
+    for (int32_t i = 0; i < E; ++i)
+        for (int32_t j = i + 1; j < E; ++j)
+            q[(int64_t)i * E + j] = (int64_t)llrint(256.0 * (double)coact_ema[(int64_t)i * E + j]);
+    for (int64_t i = 0; i < (int64_t)G * S; ++i) slot_table[i] = -1;
+
+    double W = 0.0;
+    for (int32_t e = 0; e < E; ++e) W += (double)count_ema[e];
+    double cap = (1.0 + (double)eps) * W / (double)G;
+    double node_cap = (double)g * cap;
+    int64_t all_slots = (int64_t)g * S;
+    /* slots each node keeps free through step 1 for the repair of step 2 */
+    int64_t total_need = 0;
+    for (int32_t e = 0; e < E; ++e) total_need += plan_need((double)count_ema[e], cap);
+    int64_t reserve = (int64_t)G * S > total_need ? ((int64_t)G * S - total_need) / N : 0;
+    if (reserve > g) reserve = g;
+    int64_t node_slots = all_slots - reserve;
+
+    /* experts by decreasing w, ties to the smaller id (insertion sort) */
+    for (int32_t e = 0; e < E; ++e) {
+        int32_t k = e;
+        while (k > 0 && count_ema[order[k - 1]] < count_ema[e]) {
+            order[k] = order[k - 1];
+            --k;
+        }
+        order[k] = e;
+    }
+
+    /* 1. work placement */
+    for (int32_t oi = 0; oi < E; ++oi) {
+        int32_t e = order[oi];
+        double rem = (double)count_ema[e];
+        int placed = 0, last = -1;
+        while (!placed || rem > 0.0) {
+            /* candidates with the repair reserve kept; a fitting node that
+               needs the reserved slots beats a non-fitting one */
+            int32_t best = -1, bfits = 0, broom = 0;
+            int64_t bgain = 0;
+            double bspare = 0.0;
+            int64_t slots_now = node_slots;
+            for (int32_t pass = 0; pass < 2; ++pass) {
+                int64_t lim_slots = pass == 0 ? node_slots : all_slots;
+                int32_t pb = -1, pfits = 0, proom = 0;
+                int64_t pgain = 0;
+                double pspare = 0.0;
+                for (int32_t n = 0; n < N; ++n) {
+                    if (on[(int64_t)e * N + n] || used[n] >= lim_slots) continue;
+                    int64_t nfree = lim_slots - used[n];
+                    int64_t lim = nfree < g ? nfree : g;
+                    double spare = node_cap - work[n];
+                    int fits = rem <= spare && plan_need(rem, cap) <= lim;
+                    int room = spare > 0.0;
+                    int64_t gn = plan_gain(q, on, E, N, e, n);
+                    int better = pb < 0 || fits > pfits ||
+                                 (fits == pfits && (room > proom ||
+                                  (room == proom && (spare > pspare ||
+                                   (spare == pspare && gn > pgain)))));
+                    if (better) {
+                        pb = n;
+                        pfits = fits;
+                        proom = room;
+                        pgain = gn;
+                        pspare = spare;
+                    }
+                }
+                if (pb >= 0 && (best < 0 || (pfits && !bfits))) {
+                    best = pb;
+                    bfits = pfits;
+                    broom = proom;
+                    bgain = pgain;
+                    bspare = pspare;
+                    slots_now = lim_slots;
+                }
+                if (best >= 0 && bfits) break;
+            }
+            (void)broom;
+            (void)bgain;
+            if (best < 0) {
+                if (!placed) {
+                    rc = REF_EDATA; /* no free slot left for this expert */
+                    goto done;
+                }
+                share[(int64_t)e * N + last] += rem; /* every node tried */
+                work[last] += rem;
+                rem = 0.0;
+                break;
+            }
+            int64_t nfree = slots_now - used[best];
+            int64_t lim = nfree < g ? nfree : g;
+            double take = rem;
+            if (!bfits) {
+                if (bspare < take) take = bspare;
+                if ((double)lim * cap < take) take = (double)lim * cap;
+                if (!(take > 0.0)) take = rem;
+            }
+            int64_t kk = plan_need(take, cap);
+            if (kk > lim) kk = lim;
+            on[(int64_t)e * N + best] = 1;
+            share[(int64_t)e * N + best] = take;
+            pieces[(int64_t)e * N + best] = kk;
+            used[best] += kk;
+            work[best] += take;
+            rem -= take;
+            placed = 1;
+            last = best;
+        }
+    }
+
+    /* 1b. local search over single experts */
+    for (int32_t sweep = 0; sweep < 64; ++sweep) {
+        int changed = 0;
+        for (int32_t a = 0; a < E; ++a) {
+            int32_t na = -1, cnt = 0;
+            for (int32_t n = 0; n < N; ++n)
+                if (on[(int64_t)a * N + n]) {
+                    na = n;
+                    ++cnt;
+                }
+            if (cnt != 1 || pieces[(int64_t)a * N + na] != 1) continue;
+            double wa = (double)count_ema[a];
+            int64_t ga = plan_gain(q, on, E, N, a, na);
+            int64_t bd = 0;
+            int32_t bm = -1, bb = -1;
+            for (int32_t m = 0; m < N; ++m) {
+                if (m == na || used[m] >= node_slots) continue;
+                double nw = work[m] + wa;
+                if (!(nw <= node_cap || nw <= work[m])) continue;
+                int64_t dl = plan_gain(q, on, E, N, a, m) - ga;
+                if (dl > bd) {
+                    bd = dl;
+                    bm = m;
+                }
+            }
+            for (int32_t b = 0; b < E; ++b) {
+                if (b == a) continue;
+                int32_t nb = -1, cb = 0;
+                for (int32_t n = 0; n < N; ++n)
+                    if (on[(int64_t)b * N + n]) {
+                        nb = n;
+                        ++cb;
+                    }
+                if (cb != 1 || pieces[(int64_t)b * N + nb] != 1 || nb == na) continue;
+                double wb = (double)count_ema[b];
+                double wna = work[na] - wa + wb, wnb = work[nb] - wb + wa;
+                if (!(wna <= node_cap || wna <= work[na])) continue;
+                if (!(wnb <= node_cap || wnb <= work[nb])) continue;
+                int64_t dl = plan_gain(q, on, E, N, a, nb) - ga + plan_gain(q, on, E, N, b, na) -
+                             plan_gain(q, on, E, N, b, nb) - 2 * plan_q(q, E, a, b);
+                if (dl > bd) {
+                    bd = dl;
+                    bm = -1;
+                    bb = b;
+                }
+            }
+            if (bm >= 0) {
+                on[(int64_t)a * N + na] = 0;
+                on[(int64_t)a * N + bm] = 1;
+                share[(int64_t)a * N + bm] = share[(int64_t)a * N + na];
+                share[(int64_t)a * N + na] = 0.0;
+                pieces[(int64_t)a * N + bm] = 1;
+                pieces[(int64_t)a * N + na] = 0;
+                used[na] -= 1;
+                used[bm] += 1;
+                work[na] = work[na] - wa;
+                work[bm] = work[bm] + wa;
+                changed = 1;
+            } else if (bb >= 0) {
+                int32_t nb = -1;
+                for (int32_t n = 0; n < N; ++n)
+                    if (on[(int64_t)bb * N + n]) nb = n;
+                double wb = (double)count_ema[bb];
+                on[(int64_t)a * N + na] = 0;
+                on[(int64_t)a * N + nb] = 1;
+                on[(int64_t)bb * N + nb] = 0;
+                on[(int64_t)bb * N + na] = 1;
+                share[(int64_t)a * N + nb] = share[(int64_t)a * N + na];
+                share[(int64_t)a * N + na] = 0.0;
+                share[(int64_t)bb * N + na] = share[(int64_t)bb * N + nb];
+                share[(int64_t)bb * N + nb] = 0.0;
+                pieces[(int64_t)a * N + nb] = 1;
+                pieces[(int64_t)a * N + na] = 0;
+                pieces[(int64_t)bb * N + na] = 1;
+                pieces[(int64_t)bb * N + nb] = 0;
+                work[na] = work[na] - wa + wb;
+                work[nb] = work[nb] - wb + wa;
+                changed = 1;
+            }
+        }
+        if (!changed) break;
+    }
+
+    /* 2. ranks, node by node */
+    for (int32_t n = 0; n < N; ++n) {
+        int32_t ni = 0;
+        for (int32_t e = 0; e < E; ++e) {
+            if (!on[(int64_t)e * N + n]) continue;
+            int64_t k = pieces[(int64_t)e * N + n];
+            for (int32_t c = 0; c < k; ++c) {
+                struct plan_piece it = { share[(int64_t)e * N + n] / (double)k, e, c };
+                int32_t p = ni++;
+                while (p > 0 && piece_before(&it, &items[p - 1])) {
+                    items[p] = items[p - 1];
+                    --p;
+                }
+                items[p] = it;
+            }
+        }
+        for (int32_t i = 0; i < g; ++i) rload[i] = 0.0;
+        int32_t lim = (ni + g - 1) / g;
+        if (lim > S) lim = S;
+        int stuck = 0;
+        for (int32_t t = 0; t < ni && !stuck; ++t) {
+            int32_t b = -1;
+            for (int32_t i = 0; i < g; ++i) {
+                int32_t r = n * g + i;
+                if (plan_used(slot_table, S, r) >= lim || plan_holds(slot_table, S, r, items[t].e))
+                    continue;
+                if (b < 0 || rload[i] < rload[b] ||
+                    (rload[i] == rload[b] && plan_used(slot_table, S, r) <
+                                             plan_used(slot_table, S, n * g + b)))
+                    b = i;
+            }
+            if (b < 0) {
+                stuck = 1;
+                break;
+            }
+            int32_t r = n * g + b;
+            slot_table[(int64_t)r * S + plan_used(slot_table, S, r)] = items[t].e;
+            rload[b] += items[t].load;
+            pl[(int64_t)items[t].e * G + r] += items[t].load;
+        }
+        if (stuck) {
+            for (int32_t i = 0; i < g; ++i) {
+                int32_t r = n * g + i;
+                for (int32_t k = 0; k < S; ++k) slot_table[(int64_t)r * S + k] = -1;
+                for (int32_t e = 0; e < E; ++e) pl[(int64_t)e * G + r] = 0.0;
+            }
+            int64_t kmax = 0;
+            for (int32_t e = 0; e < E; ++e)
+                if (on[(int64_t)e * N + n] && pieces[(int64_t)e * N + n] > kmax)
+                    kmax = pieces[(int64_t)e * N + n];
+            int32_t p = 0;
+            for (int64_t k = kmax; k >= 1; --k)
+                for (int32_t e = 0; e < E; ++e) {
+                    if (!on[(int64_t)e * N + n] || pieces[(int64_t)e * N + n] != k) continue;
+                    for (int64_t c = 0; c < k; ++c) {
+                        int32_t r = n * g + p % g;
+                        slot_table[(int64_t)r * S + plan_used(slot_table, S, r)] = e;
+                        pl[(int64_t)e * G + r] += share[(int64_t)e * N + n] / (double)k;
+                        ++p;
+                    }
+                }
+        }
+        /* repair: augmenting paths from the most loaded rank */
+        for (int64_t moves = 0; moves < 4 * (int64_t)g * g * S; ++moves) {
+            int32_t h = -1;
+            double hl = 0.0;
+            for (int32_t i = 0; i < g; ++i) {
+                double l = plan_rank_load(pl, E, G, n * g + i);
+                if (h < 0 || l > hl) {
+                    h = i;
+                    hl = l;
+                }
+            }
+            if (!(hl > cap)) break;
+            int32_t queue[32], parent[32], via[32];
+            uint8_t seen[32] = { 0 };
+            int32_t qh = 0, qt = 0, target = -1;
+            queue[qt++] = h;
+            seen[h] = 1;
+            while (qh < qt && target < 0) {
+                int32_t a = queue[qh++], ra = n * g + a;
+                for (int32_t e = 0; e < E && target < 0; ++e) {
+                    if (!(pl[(int64_t)e * G + ra] > 0.0)) continue;
+                    for (int32_t b = 0; b < g && target < 0; ++b) {
+                        int32_t rb = n * g + b;
+                        if (seen[b]) continue;
+                        if (!plan_holds(slot_table, S, rb, e) && plan_used(slot_table, S, rb) >= S)
+                            continue;
+                        seen[b] = 1;
+                        parent[b] = a;
+                        via[b] = e;
+                        queue[qt++] = b;
+                        if (plan_rank_load(pl, E, G, rb) < cap) target = b;
+                    }
+                }
+            }
+            if (target < 0) {
+                /* slot swap: the heaviest expert eh on h (ties smaller e);
+                   under-cap ranks u without a free slot and without eh, in
+                   increasing load (ties smaller); on u, the expert x with
+                   least work (ties smaller) that h does not hold and whose
+                   work is below eh's on h. x moves whole to h, then
+                   min(load_h - cap + w_x, cap - load_u + w_x, l_eh,h) of
+                   eh moves to u. Needs a free slot on h. */
+                int32_t rh = n * g + h;
+                if (plan_used(slot_table, S, rh) >= S) break;
+                int32_t eh = -1;
+                for (int32_t k = 0; k < S; ++k) {
+                    int32_t x = slot_table[(int64_t)rh * S + k];
+                    if (x < 0) continue;
+                    if (eh < 0 || pl[(int64_t)x * G + rh] > pl[(int64_t)eh * G + rh] ||
+                        (pl[(int64_t)x * G + rh] == pl[(int64_t)eh * G + rh] && x < eh))
+                        eh = x;
+                }
+                double weh = pl[(int64_t)eh * G + rh];
+                int32_t bu = -1, bx = -1;
+                double bul = 0.0;
+                for (int32_t u = 0; u < g; ++u) {
+                    int32_t ru = n * g + u;
+                    double lu = plan_rank_load(pl, E, G, ru);
+                    if (u == h || !(lu < cap) || plan_used(slot_table, S, ru) < S ||
+                        plan_holds(slot_table, S, ru, eh))
+                        continue;
+                    int32_t x = -1;
+                    for (int32_t k = 0; k < S; ++k) {
+                        int32_t y = slot_table[(int64_t)ru * S + k];
+                        if (y < 0 || plan_holds(slot_table, S, rh, y)) continue;
+                        if (!(pl[(int64_t)y * G + ru] < weh)) continue;
+                        if (x < 0 || pl[(int64_t)y * G + ru] < pl[(int64_t)x * G + ru] ||
+                            (pl[(int64_t)y * G + ru] == pl[(int64_t)x * G + ru] && y < x))
+                            x = y;
+                    }
+                    if (x < 0) continue;
+                    if (bu < 0 || lu < bul) {
+                        bu = u;
+                        bx = x;
+                        bul = lu;
+                    }
+                }
+                if (bu < 0) break;
+                int32_t ru = n * g + bu;
+                double wx = pl[(int64_t)bx * G + ru];
+                double mv = hl - cap + wx;
+                if (cap - bul + wx < mv) mv = cap - bul + wx;
+                if (weh < mv) mv = weh;
+                if (!(mv > wx)) break;
+                /* x: off u (slots stay packed), onto h */
+                int32_t k = 0;
+                while (slot_table[(int64_t)ru * S + k] != bx) ++k;
+                for (; k + 1 < S; ++k) slot_table[(int64_t)ru * S + k] = slot_table[(int64_t)ru * S + k + 1];
+                slot_table[(int64_t)ru * S + S - 1] = -1;
+                slot_table[(int64_t)rh * S + plan_used(slot_table, S, rh)] = bx;
+                pl[(int64_t)bx * G + ru] = 0.0;
+                pl[(int64_t)bx * G + rh] += wx;
+                /* part of eh: off h, onto u */
+                slot_table[(int64_t)ru * S + plan_used(slot_table, S, ru)] = eh;
+                pl[(int64_t)eh * G + rh] -= mv;
+                pl[(int64_t)eh * G + ru] += mv;
+                continue;
+            }
+            double mv = hl - cap;
+            double room = cap - plan_rank_load(pl, E, G, n * g + target);
+            if (room < mv) mv = room;
+            for (int32_t b = target; b != h; b = parent[b]) {
+                double avail = pl[(int64_t)via[b] * G + n * g + parent[b]];
+                if (avail < mv) mv = avail;
+            }
+            if (!(mv > cap * 1e-12)) break;
+            for (int32_t b = target; b != h; b = parent[b]) {
+                int32_t e = via[b], ra = n * g + parent[b], rb = n * g + b;
+                if (!plan_holds(slot_table, S, rb, e))
+                    slot_table[(int64_t)rb * S + plan_used(slot_table, S, rb)] = e;
+                pl[(int64_t)e * G + ra] -= mv;
+                pl[(int64_t)e * G + rb] += mv;
+            }
+        }
+        used[n] = 0;
+        for (int32_t i = 0; i < g; ++i) used[n] += plan_used(slot_table, S, n * g + i);
+    }
+
+    /* 3. co-activation replicas */
+    for (;;) {
+        int32_t be = -1, bn = -1;
+        int64_t bg = 0;
+        for (int32_t e = 0; e < E; ++e)
+            for (int32_t n = 0; n < N; ++n) {
+                if (on[(int64_t)e * N + n] || used[n] >= all_slots) continue;
+                int64_t gn = plan_gain(q, on, E, N, e, n);
+                if (gn <= 0) continue;
+                if (be < 0 || gn > bg || (gn == bg && count_ema[e] > count_ema[be])) {
+                    be = e;
+                    bn = n;
+                    bg = gn;
+                }
+            }
+        if (be < 0) break;
+        int32_t b = -1;
+        for (int32_t i = 0; i < g; ++i) {
+            int32_t r = bn * g + i;
+            if (plan_used(slot_table, S, r) >= S) continue;
+            if (b < 0 || plan_used(slot_table, S, r) < plan_used(slot_table, S, bn * g + b)) b = i;
+        }
+        int32_t r = bn * g + b;
+        slot_table[(int64_t)r * S + plan_used(slot_table, S, r)] = be;
+        on[(int64_t)be * N + bn] = 1;
+        used[bn] += 1;
+    }
+
+    /* owners, plan, objective, feasibility */
+    for (int32_t e = 0; e < E; ++e) {
+        owner[e] = -1;
+        for (int32_t r = 0; r < G; ++r)
+            if (plan_holds(slot_table, S, r, e) &&
+                (owner[e] < 0 || pl[(int64_t)e * G + r] > pl[(int64_t)e * G + owner[e]]))
+                owner[e] = r;
+    }
+    if (plan)
+        for (int64_t i = 0; i < (int64_t)E * G; ++i) plan[i] = (float)pl[i];
+    if (objective) {
+        int64_t obj = 0;
+        for (int32_t n = 0; n < N; ++n)
+            for (int32_t i = 0; i < E; ++i)
+                for (int32_t j = i + 1; j < E; ++j)
+                    if (on[(int64_t)i * N + n] && on[(int64_t)j * N + n]) obj += q[(int64_t)i * E + j];
+        *objective = (double)obj / 256.0;
+    }
+    if (feasible) {
+        int ok = 1;
+        for (int32_t r = 0; r < G; ++r)
+            if (plan_rank_load(pl, E, G, r) > cap * (1.0 + 1e-9)) ok = 0;
+        *feasible = ok;
+    }
+done:
+    free(q); free(on); free(share); free(pieces); free(order); free(used); free(work); free(pl);
+    free(items); free(rload); free(dest);
+    return rc;
+}
