@@ -261,6 +261,41 @@ cobalt_status cobalt_intra_node_rebalance(int32_t N, int32_t gpus_per_node, int3
                                           int32_t* host_new_owner_rank, float* host_rank_load);
 
 /* ------------------------------------------------------------------------
+ * Periodic global planning (Section 3.2, Stage 1; Eq. 3), host only.
+ *
+ * Chooses a replica layout and a division of each expert's estimated work
+ * over its replicas that keep co-activated experts on the same node:
+ * maximise sum_n sum_{i<j} c_ij [i and j both on node n] with every expert
+ * placed, at most S replicas per rank, no expert twice on a rank, and at
+ * most cap = (1 + eps) W / G planned work per rank, W = sum_e w_e. The
+ * paper solves this as a MILP; this is a deterministic greedy heuristic for
+ * the same objective and constraints (work placement on nodes by longest
+ * processing time, moves and swaps that raise the objective, rank packing
+ * with augmenting-path repair of the work division, then replicas that
+ * raise the objective in the remaining slots). Pair weights are quantised
+ * to 1/256 so that every comparison of gains is exact.
+ *
+ * host_coact_ema [E][E] fp32 in: c_ij (EMA of co-activation counts; only
+ *   i < j is read; finite, >= 0, <= 2^40).
+ * host_count_ema [E] fp32 in: w_e (EMA of expert task counts; finite, >= 0).
+ * eps: the allowed imbalance (>= 0; the paper's default is 0.15).
+ * host_slot_table [G][S] int32 out: expert ids, -1 for empty slots.
+ * host_owner_rank [E] int32 out: the rank with the most planned work.
+ * host_plan [E][G] fp32 out (may be NULL): planned work w'_er, which can
+ *   initialise Stage 2's replica-level EMA.
+ * host_objective (may be NULL): the objective, from the quantised weights.
+ * host_feasible (may be NULL): 1 if every rank's planned work is within
+ *   cap (1 + 1e-9), else 0 (the heuristic found no division within cap).
+ * Returns COBALT_EINVAL for bad sizes, G*S < E or a bad eps, COBALT_EDATA
+ * for bad statistics or when some expert finds no free slot.
+ * ---------------------------------------------------------------------- */
+cobalt_status cobalt_plan_layout(int32_t N, int32_t gpus_per_node, int32_t E, int32_t S,
+                                 const float* host_coact_ema, const float* host_count_ema,
+                                 float eps, int32_t* host_slot_table, int32_t* host_owner_rank,
+                                 float* host_plan, double* host_objective,
+                                 int32_t* host_feasible);
+
+/* ------------------------------------------------------------------------
  * Planner statistics (Section 3.2): exponential moving averages of the
  * step's counts, and the Ochiai similarity of expert pairs (Section 1, the
  * footnote on Fig. 3). The paper gives no decay; it is a parameter.

@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
         "cobalt_replica_load_workspace_bytes": ([i64, i32, i32, i32], sz),
         "cobalt_replica_load": ([P, P, i64, i32, i32, i32, P, P, sz, P], ctypes.c_int),
         "cobalt_intra_node_rebalance": ([i32, i32, i32, i32, P, P, P, P, P, P], ctypes.c_int),
+        "cobalt_plan_layout": ([i32, i32, i32, i32, P, P, ctypes.c_float, P, P, P, P, P],
+                               ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -295,6 +297,32 @@ def cobalt_intra_node_rebalance(N: int, gpus_per_node: int, E: int, S: int, slot
           None if own is None else own.ctypes.data_as(P), rl.ctypes.data_as(P),
           out.ctypes.data_as(P), new_own.ctypes.data_as(P), rank_load.ctypes.data_as(P))
     return out, new_own, rank_load
+
+
+def cobalt_plan_layout(N: int, gpus_per_node: int, E: int, S: int, coact_ema, count_ema,
+                       eps: float = 0.15):
+    """Host-only Stage-1 planner. Returns (slot_table [G, S] int32,
+    owner_rank [E] int32, plan [E, G] float32, objective float, feasible
+    bool). coact_ema [E, E] and count_ema [E] are host arrays or tensors."""
+    G = N * gpus_per_node
+    if isinstance(coact_ema, torch.Tensor):
+        coact_ema = coact_ema.detach().cpu().numpy()
+    if isinstance(count_ema, torch.Tensor):
+        count_ema = count_ema.detach().cpu().numpy()
+    c = np.ascontiguousarray(coact_ema, dtype=np.float32)
+    w = np.ascontiguousarray(count_ema, dtype=np.float32)
+    if c.shape != (E, E) or w.shape != (E,):
+        raise ValueError(f"coact_ema must be [{E}, {E}] and count_ema [{E}]")
+    table = np.zeros((G, S), np.int32)
+    owner = np.zeros(E, np.int32)
+    plan = np.zeros((E, G), np.float32)
+    obj = ctypes.c_double()
+    feas = ctypes.c_int32()
+    P = ctypes.c_void_p
+    _call("cobalt_plan_layout", N, gpus_per_node, E, S, c.ctypes.data_as(P), w.ctypes.data_as(P),
+          float(eps), table.ctypes.data_as(P), owner.ctypes.data_as(P), plan.ctypes.data_as(P),
+          ctypes.byref(obj), ctypes.byref(feas))
+    return table, owner, plan, obj.value, bool(feas.value)
 
 
 def replica_load_workspace_for(T: int, K: int, E: int, G: int, device="cuda") -> torch.Tensor:
