@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--cpu-sample-tokens", type=int, default=65536)
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the extra timing of the step replayed as a HIP graph")
+    ap.add_argument("--replan", choices=("planner", "recipe"), default="planner",
+                    help="multi-step workloads: re-plan the layout with the Stage-1 planner "
+                         "from the EMA statistics, or with the workload's hot-order recipe")
     return ap.parse_args()
 
 
@@ -53,6 +56,8 @@ def algorithmic_bytes(w):
     T, K, d, E, G = w.T, w.K, w.d, w.E, w.G
     return {
         "cobalt_coact_stats": T * K * 4 + 2 * 4 * (E * E + E),
+        # counts read and cleared, EMA read and written, Ochiai written
+        "cobalt_coact_ema": E * E * 4 * 5 + E * 4 * 4,
         "cobalt_assign": T * K * 4 + T * K * 4 + T * 2,
         "cobalt_dispatch_pack": T * d * 2 + T * K * d * 2 + T * K * 8 + 12 * G * G,
         "cobalt_combine": T * K * d * 2 + T * K * 8 + T * d * 2,
@@ -149,6 +154,47 @@ def stage2_demo(st, torch, B, W):
             "imbalance_after": float(after.max() / mean), "host_ms": host_ms}
 
 
+def stage1_demo(st, torch, B):
+    """Periodic global planning (Section 3.2, Stage 1) from the EMAs the GPU
+    keeps: the host planner turns ema_coact / ema_count into a layout, and
+    this step is re-assigned on it with Algorithm 1. Reports Eq. 1's V and
+    the rank-load imbalance (max / mean) against the current layout, then
+    after one Stage-2 rebalance of the planned layout on its measured
+    replica loads."""
+    import numpy as np
+    w = st.w
+
+    def measure(table, owner):
+        L = B.cobalt_layout_create(w.N, w.g, w.E, table.shape[1], table, owner)
+        a = torch.empty_like(st.assigned)
+        rn = torch.empty_like(st.remote)
+        B.cobalt_assign(L, st.topk, st.src, st.seed, st.step, 0, a, rn)
+        load = torch.zeros(w.E, w.G, dtype=torch.int32, device="cuda")
+        B.cobalt_replica_load(st.topk, a, w.E, w.G, load, st.load_workspace)
+        torch.cuda.synchronize()
+        B.cobalt_layout_destroy(L)
+        rn32 = rn.to(torch.int32) & 0xFFFF
+        V = sum(((rn32 >> n) & 1).sum().item() for n in range(w.N))
+        per_rank = torch.bincount(a.flatten().long(), minlength=w.G).float()
+        return int(V), float(per_rank.max() / per_rank.mean()), load.cpu().numpy().view(np.uint32)
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    table, owner, plan, obj, feasible = B.cobalt_plan_layout(
+        w.N, w.g, w.E, w.S, st.ema_coact, st.ema_count, 0.15)
+    host_ms = (time.perf_counter() - t0) * 1e3
+    V0, imb0, _ = measure(st.table, st.owner)
+    V1, imb1, rl = measure(table, owner)
+    t2, o2, _ = B.cobalt_intra_node_rebalance(w.N, w.g, w.E, table.shape[1], table, owner,
+                                              rl.astype(np.float32))
+    V2, imb2, _ = measure(t2, o2)
+    return {"eps": 0.15, "objective": obj, "plan_within_cap": feasible,
+            "planner_host_ms": host_ms,
+            "current_layout": {"V": V0, "imbalance": imb0},
+            "planned_layout": {"V": V1, "imbalance": imb1},
+            "planned_then_stage2": {"V": V2, "imbalance": imb2}}
+
+
 def cpu_baseline(st, n_tokens, torch, W, PL):
     """The oracle, as it stands, on the first n_tokens of the same workload,
     in chunks of 4096 tokens (each chunk a full pass: stats, assign, dispatch
@@ -206,6 +252,15 @@ def main():
     stream = torch.cuda.Stream()
     calls = ["cobalt_coact_stats", "cobalt_assign", "cobalt_dispatch_pack", "cobalt_combine"]
     fns = [st.stats, st.assign, st.pack, st.combine]
+    drift = w.steps > 1
+    planner = drift and args.replan == "planner"
+    if planner:
+        # the step also folds its counts into the planner EMAs (and clears
+        # them), which the Stage-1 planner reads before the swap step
+        def ema_step(stream=None):
+            st.ema(0.9, B.EMA_CLEAR | (B.EMA_INIT if st.step == 0 else 0), stream=stream)
+        calls.insert(1, "cobalt_coact_ema")
+        fns.insert(1, ema_step)
 
     # a streaming kernel of known size (reads 1 GiB, writes 1 GiB), the
     # reference against which HBM counter readings are scaled
@@ -227,7 +282,22 @@ def main():
     # statistics accumulate over a cycle and the replicas are re-planned
     # from them before the swap step. The re-plan is host work between
     # steps, so such runs are timed by the sum of per-step HIP events.
-    drift = w.steps > 1
+    plan_info = []
+
+    def replan(s):
+        """The layout swap before step s: the Stage-1 planner on the EMAs, or
+        the workload's hot-order recipe on the accumulated expert counts."""
+        if planner:
+            tp = time.perf_counter()
+            table, owner, _, obj, within = B.cobalt_plan_layout(
+                w.N, w.g, w.E, w.S, st.ema_coact, st.ema_count, 0.15)
+            plan_info.append(((time.perf_counter() - tp) * 1e3, obj, within))
+            st.set_layout(table, owner)
+        else:
+            counts = st.count.cpu().numpy().view("uint32").astype("int64")
+            hot = sorted(range(w.E), key=lambda e: (-counts[e], e))
+            st.set_layout(*W.layout(w, seed, hot_order=hot, plan=s))
+
     if drift:
         routes = [W.routing(w, seed, step=s, device="cuda") for s in range(w.steps)]
         first_layout = (st.table, st.owner)
@@ -248,9 +318,7 @@ def main():
                     st.set_layout(*first_layout)
                 if s == w.swap_step:
                     stream.synchronize()
-                    counts = st.count.cpu().numpy().view("uint32").astype("int64")
-                    hot = sorted(range(w.E), key=lambda e: (-counts[e], e))
-                    st.set_layout(*W.layout(w, seed, hot_order=hot, plan=s))
+                    replan(s)
                 st.topk, st.gates = routes[s]
                 st.step = s
             e = evs[k]
@@ -273,7 +341,7 @@ def main():
     traffic = measured_traffic(dominant, wl_name)
     pc_bytes = ab["cobalt_dispatch_pack"] + ab["cobalt_combine"]
     pc_s = (call_ms["cobalt_dispatch_pack"] + call_ms["cobalt_combine"]) * 1e-3
-    step_bytes = sum(ab.values())
+    step_bytes = sum(ab[c] for c in calls)
 
     result = {
         "metric": METRIC,
@@ -291,7 +359,10 @@ def main():
         "config": {"workload": f"co-activation routing step, {w.describe()}, "
                                f"{w.name}, seed {seed}" +
                                (f", {w.steps}-step drift cycle with re-plan before step "
-                                f"{w.swap_step}, timed by per-step events" if drift else ""),
+                                f"{w.swap_step} by the " +
+                                ("Stage-1 planner from the EMA statistics (EMA update in "
+                                 "each step)" if planner else "hot-order recipe") +
+                                ", timed by per-step events" if drift else ""),
                    "T": w.T, "E": w.E, "K": w.K, "d": w.d, "nodes": w.N,
                    "gpus_per_node": w.g, "slots_per_gpu": w.S,
                    "parallelism": "single GPU; virtual ranks are HBM buffers"},
@@ -303,6 +374,36 @@ def main():
         "call_ms": call_ms,
         "call_gbps": {c: ab[c] / (call_ms[c] * 1e-3) / 1e9 for c in calls},
     }
+    if drift:
+        # one more cycle, untimed, recording Eq. 1's V and the rank-load
+        # imbalance of every step on the layout the cycle's re-plan chose
+        st.set_layout(*first_layout)
+        st.coact.zero_()
+        st.count.zero_()
+        per_step = []
+        for s_ in range(w.steps):
+            if s_ == w.swap_step:
+                torch.cuda.synchronize()
+                replan(s_)
+            st.topk, st.gates = routes[s_]
+            st.step = s_
+            for f in fns[:-2]:  # statistics, EMA and assignment
+                f()
+            rn32 = st.remote.to(torch.int32) & 0xFFFF
+            V = sum(((rn32 >> n) & 1).sum().item() for n in range(w.N))
+            per_rank = torch.bincount(st.assigned.flatten().long(), minlength=w.G).float()
+            per_step.append((int(V), float(per_rank.max() / per_rank.mean())))
+        before, after = per_step[:w.swap_step], per_step[w.swap_step:]
+        result["replan"] = {"method": "stage1_planner" if planner else "hot_order_recipe",
+                            "before_step": w.swap_step,
+                            "mean_V_before": sum(v for v, _ in before) / len(before),
+                            "mean_V_after": sum(v for v, _ in after) / len(after),
+                            "mean_imbalance_before": sum(i for _, i in before) / len(before),
+                            "mean_imbalance_after": sum(i for _, i in after) / len(after)}
+        if plan_info:
+            result["replan"].update({
+                "planner_host_ms": sum(p[0] for p in plan_info) / len(plan_info),
+                "objective": plan_info[-1][1], "plan_within_cap": plan_info[-1][2]})
     if not drift and not args.no_graph:
         # the same four calls captured once as a HIP graph and replayed
         g = torch.cuda.CUDAGraph()
@@ -384,6 +485,7 @@ def main():
             float(st.ochiai[pairs & ~same].mean().item())
     result["routing"] = routing_quality(st, torch, B, W)
     result["routing"]["stage2_rebalance"] = stage2_demo(st, torch, B, W)
+    result["routing"]["stage1_plan"] = stage1_demo(st, torch, B)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(st, args.cpu_sample_tokens, torch, W, PL)
     st.close()

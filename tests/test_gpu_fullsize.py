@@ -116,3 +116,50 @@ def test_drift_sixteen_steps_with_layout_swap():
     st.close()
     del st
     torch.cuda.empty_cache()
+
+
+def test_drift_cycle_with_the_stage1_planner():
+    """The method's own loop over the drift workload's 16 steps (T=262144,
+    E=384): each step's counts fold into the EMAs on the GPU and are
+    cleared; before step 8 the host planner turns the EMAs into a new
+    layout; Algorithm 1 and the dispatch layout run on it. The oracle runs
+    the same loop from its own counts; every integer output, the EMAs and
+    the planned layout agree exactly."""
+    w = W.WORKLOADS["drift-e384"]
+    seed = w.seed
+    st = PL.RoutingStep(w, seed=seed, device="cuda")
+    ref_c = np.zeros((w.E, w.E), np.float32)
+    ref_n = np.zeros(w.E, np.float32)
+    tabs = oracle.layout_tables(w.N, w.g, w.E, st.table, st.owner)
+    for step in range(w.steps):
+        if step > 0:
+            st.set_routing(step)
+        topk = st.topk.cpu().numpy()
+        if step == w.swap_step:
+            got = B.cobalt_plan_layout(w.N, w.g, w.E, w.S, st.ema_coact, st.ema_count, 0.15)
+            want = oracle.plan_layout(w.N, w.g, w.E, w.S, ref_c, ref_n, 0.15)
+            for x, y in zip(got[:3], want[:3]):
+                assert np.array_equal(x, y), "planned layout differs"
+            assert got[3] == want[3] and got[4] == want[4]
+            st.set_layout(got[0], got[1])
+            tabs = oracle.layout_tables(w.N, w.g, w.E, want[0], want[1])
+        st.stats()
+        st.ema(0.9, B.EMA_CLEAR | (B.EMA_INIT if step == 0 else 0))
+        st.assign()
+        st.pack()
+        torch.cuda.synchronize()
+        print(f"planner cycle step {step}", flush=True)
+        C, n = oracle.coact_stats(topk, w.E)
+        oracle.count_ema(C, 0.9, ema=ref_c, init=step == 0)
+        oracle.count_ema(n, 0.9, ema=ref_n, init=step == 0)
+        assert np.array_equal(st.ema_coact.cpu().numpy().view(np.uint32), ref_c.view(np.uint32))
+        assert np.array_equal(st.ema_count.cpu().numpy().view(np.uint32), ref_n.view(np.uint32))
+        a, rn = oracle.assign(w.N, w.g, w.E, tabs, topk, None, seed=seed, step=step)
+        assert np.array_equal(st.assigned.cpu().numpy(), a), f"assignment differs at {step}"
+        assert np.array_equal(st.remote.cpu().numpy().view(np.uint16), rn)
+        counts, offsets, pos, _ = oracle.dispatch(a, w.G)
+        assert np.array_equal(st.offsets.cpu().numpy(), offsets)
+        assert np.array_equal(st.pos.cpu().numpy(), pos)
+    st.close()
+    del st
+    torch.cuda.empty_cache()
