@@ -37,11 +37,17 @@ _lib = None
 
 
 def lib():
+    """The oracle library. ORACLE_LIB names another build of it to load
+    instead; the planted-mistake tests use it to run the pins against
+    deliberately broken copies of the oracle."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH) or os.path.getmtime(LIB_PATH) < os.path.getmtime(SRC_PATH):
-            build()
-        L = ctypes.CDLL(LIB_PATH)
+        path = os.environ.get("ORACLE_LIB")
+        if path is None:
+            path = LIB_PATH
+            if not os.path.exists(LIB_PATH) or os.path.getmtime(LIB_PATH) < os.path.getmtime(SRC_PATH):
+                build()
+        L = ctypes.CDLL(path)
         P = ctypes.c_void_p
         i32, i64, u32, u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64
         L.ref_splitmix64.argtypes = [u64]

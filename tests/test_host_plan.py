@@ -61,6 +61,9 @@ def test_structured_cases():
     w[5] = 20.0
     same(4, 2, 16, 4, np.zeros((16, 16), np.float32), w, 0.15)
     same(2, 2, 8, 2, np.zeros((8, 8), np.float32), np.zeros(8, np.float32), 0.15)
+    c = np.zeros((4, 4), np.float32)
+    c[0, 1] = c[1, 0] = 100.0
+    assert same(2, 1, 4, 2, c, np.array([3, 3, 1, 1], np.float32), 0.15)[4]
 
 
 def test_library_rejects_what_the_oracle_rejects():

@@ -163,3 +163,19 @@ def test_beats_the_recipe_layout_on_planted_clusters():
         a, _ = oracle.assign(w.N, w.g, w.E, tabs, topk, seed=1)
         V.append(oracle.traffic(a, w.N, w.g)[0])
     assert V[1] < 0.9 * V[0]
+
+
+def test_work_cap_overrides_co_activation():
+    """Two heavy experts (work 3 each) co-activate strongly, two light ones
+    (work 1) not at all, on two one-rank nodes with two slots: together the
+    heavy pair would need 6 > cap = 1.15 * 8 / 2 = 4.6, so Eq. 3's balance
+    constraint keeps them apart, and every plan step must respect it."""
+    N, g, S, E = 2, 1, 2, 4
+    w = np.array([3, 3, 1, 1], np.float32)
+    c = np.zeros((E, E), np.float32)
+    c[0, 1] = c[1, 0] = 100.0
+    out = oracle.plan_layout(N, g, E, S, c, w, 0.15)
+    held, on, loads, cap = check_solution(N, g, E, S, c, w, 0.15, out)
+    assert out[4], "a division within the cap exists: one heavy expert per node"
+    assert loads.max() <= cap
+    assert held.sum() == E and not (on[0] & on[1]).any()  # no spare slot: apart
