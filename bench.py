@@ -126,6 +126,32 @@ def routing_quality(st, torch, B, W):
     return out
 
 
+def hbm_reference(torch, stream, reps=5):
+    """Measured HBM rates of plain torch kernels on 4 GiB buffers, on the
+    bench's stream: a fill (write only), a sum (read only) and a copy (read
+    and write). They show what a simple streaming kernel reaches on this
+    device, beside the 8 TB/s peak."""
+    n = 1 << 30  # int32 elements: 4 GiB
+    a = torch.ones(n, dtype=torch.int32, device="cuda")
+    b = torch.empty_like(a)
+    out = {}
+    with torch.cuda.stream(stream):
+        for name, fn, nbytes in (("write_fill", lambda: b.fill_(3), 4 * n),
+                                 ("read_sum", lambda: a.sum(), 4 * n),
+                                 ("copy", lambda: b.copy_(a), 8 * n)):
+            fn()
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev[0].record(stream)
+            for _ in range(reps):
+                fn()
+            ev[1].record(stream)
+            torch.cuda.synchronize()
+            out[name] = nbytes / (ev[0].elapsed_time(ev[1]) / reps * 1e-3) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return {k: round(v, 1) for k, v in out.items()} | {"unit": "GB/s", "buffer": "4 GiB int32"}
+
+
 def stage2_demo(st, torch, B, W):
     """Per-step intra-node rebalancing (Section 3.2, Stage 2) on this step:
     the per-replica loads w_er measured on the GPU drive the host greedy
@@ -431,6 +457,12 @@ def main():
         ev[1].record(stream)
     torch.cuda.synchronize()
     result["extra_calls_ms"] = {"cobalt_replica_load": ev[0].elapsed_time(ev[1]) / args.steps}
+    ref = hbm_reference(torch, stream)
+    result["hbm_reference"] = ref
+    result["call_frac_of_reference"] = {
+        "cobalt_dispatch_pack_vs_write_fill":
+            result["call_gbps"]["cobalt_dispatch_pack"] / ref["write_fill"],
+        "cobalt_combine_vs_copy": result["call_gbps"]["cobalt_combine"] / ref["copy"]}
     # the node-deduplicated dispatch of the last step's assignment: one row
     # per (token, destination node) instead of one per (token, expert)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]

@@ -19,8 +19,9 @@
 //   rank   per tile: wave multi-split ranks (ballots over the bits of r),
 //          per-wave running counts in LDS, aggregates published, look-back
 //          over predecessor tiles per destination, then pos
-//   copy   each wave reads a 1-2 KiB slice of one token row of x once
-//          into registers and stores it to the token's K packed rows
+//   scatter one wave per (token, 2 KiB slice, slot): reads the slice of x
+//          (from the cache for all but the first of the token's K waves)
+//          and stores it to the slot's packed row
 //
 // The node-deduplicated layout (Section 1, Eq. 1: a token crosses to a node
 // once and is forwarded inside it) has one row per (token, destination node)
@@ -28,7 +29,9 @@
 //     node_pos[t][n] = offsets[s][n] - colprefix[s][n] + prefix_n(t),
 // where prefix_n(t) counts the tokens before t that reach node n: an N-way
 // prefix count over tokens, done with ballots per node bit and the same
-// decoupled look-back. The same init, scan and copy kernels serve both.
+// decoupled look-back. The same init and scan kernels serve both; the node
+// rows are written by copy_kernel, one wave storing its slice of x[t] to all
+// of the token's node rows.
 #include <algorithm>
 
 #include "internal.hpp"
@@ -509,6 +512,58 @@ __global__ __launch_bounds__(kRankThreads) void node_rank_kernel(
     }
 }
 
+// Row scatter for the per-pair layout: one workgroup per (token, 2 KiB
+// column slice), one wave per slot j. The K waves that copy one slice of
+// x[t] share a workgroup, so the slice is read from HBM once and from the
+// cache K - 1 times (plain loads keep it cached); each wave then issues a
+// single 2 KiB burst to one packed row, with non-temporal stores. On the
+// T=131072, K=8, d=7168 workload this reaches 5.7 TB/s, where the fan-out
+// of copy_kernel (one wave stores its slice to all K rows) reaches 5.1.
+// GROUPS, the number of slices per row, is a template parameter so that
+// the block index splits into (token, slice) with a constant division: a
+// wave does two loads and two stores, and a runtime 64-bit division would
+// cost it more scalar instructions than that.
+template <int GROUPS>
+__global__ __launch_bounds__(kMaxK * 64) void scatter_kernel(
+    const u32x4* __restrict__ x, const int32_t* __restrict__ pos, int K, int64_t nch,
+    int64_t TK, u32x4* __restrict__ packed) {
+    const uint32_t tg = blockIdx.x;
+    const uint32_t t = tg / GROUPS;
+    const uint32_t g = tg - t * GROUPS;
+    const int j = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t c0 = (int64_t)g * 128 + (threadIdx.x & 63);
+    // The x loads are issued before the packed row is read: a branch on the
+    // row first would make every wave wait for that load before its own
+    // two loads start (measured: 3.45 ms instead of 2.95 ms).
+    const u32x4* row = x + (int64_t)t * nch;
+    const bool in0 = c0 < nch, in1 = c0 + 64 < nch;
+    u32x4 v0, v1;
+    if (in0) v0 = row[c0];
+    if (in1) v1 = row[c0 + 64];
+    const int p = pos[(int64_t)t * K + j];
+    if (p < 0 || p >= TK) return;
+    u32x4* dst = packed + (int64_t)p * nch;
+    if (in0) __builtin_nontemporal_store(v0, dst + c0);
+    if (in1) __builtin_nontemporal_store(v1, dst + c0 + 64);
+}
+
+// Launches scatter_kernel when the slice count has an instantiation and
+// the block count fits; returns false otherwise (the caller then uses the
+// fan-out copy).
+template <int GROUPS>
+bool try_scatter(const void* x, const int32_t* pos, int64_t T, int K, int64_t nch,
+                 void* packed, hipStream_t s) {
+    if ((nch + 127) / 128 != GROUPS) return try_scatter<GROUPS - 1>(x, pos, T, K, nch, packed, s);
+    if (T * GROUPS >= (int64_t(1) << 31)) return false;
+    hipLaunchKernelGGL(scatter_kernel<GROUPS>, dim3((unsigned)(T * GROUPS)), dim3(K * 64), 0, s,
+                       (const u32x4*)x, pos, K, nch, T * K, (u32x4*)packed);
+    return true;
+}
+template <>
+bool try_scatter<0>(const void*, const int32_t*, int64_t, int, int64_t, void*, hipStream_t) {
+    return false;
+}
+
 // Copies x[t] to the rows pos[t][0..per_tok) that are in [0, bound).
 template <bool kNode>
 cobalt_status launch_copy(const void* x, const int32_t* pos, int64_t T, int per_tok, int64_t d,
@@ -593,6 +648,10 @@ cobalt_status launch_dispatch(const int32_t* assigned, const int32_t* src, int64
                        src, K, G, tok_per_src, TK, w.ntiles, w.ctrl, w.base, w.status, pos);
     COBALT_LAUNCH_CHECK();
     if (!x) return COBALT_OK;
+    if (try_scatter<16>(x, pos, T, K, d / 8, packed, s)) {
+        COBALT_LAUNCH_CHECK();
+        return COBALT_OK;
+    }
     return launch_copy<false>(x, pos, T, K, d, TK, packed, s);
 }
 
