@@ -514,7 +514,7 @@ def main():
         result["planner_statistics"]["ochiai_mean_planted_cluster_pairs"] = \
             float(st.ochiai[inside].mean().item())
         result["planner_statistics"]["ochiai_mean_other_pairs"] = \
-            float(st.ochiai[pairs & ~same].mean().item())
+            float(st.ochiai[pairs & same.logical_not()].mean().item())
     result["routing"] = routing_quality(st, torch, B, W)
     result["routing"]["stage2_rebalance"] = stage2_demo(st, torch, B, W)
     result["routing"]["stage1_plan"] = stage1_demo(st, torch, B)
