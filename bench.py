@@ -126,6 +126,17 @@ def routing_quality(st, torch, B, W):
     return out
 
 
+def device_info(torch):
+    """hipDeviceProp of device 0, as torch reports it."""
+    p = torch.cuda.get_device_properties(0)
+    out = {"name": p.name, "compute_units": p.multi_processor_count,
+           "hbm_bytes": p.total_memory}
+    for k in ("gcnArchName", "L2_cache_size"):
+        if hasattr(p, k):
+            out[k] = getattr(p, k)
+    return out
+
+
 def hbm_reference(torch, stream, reps=5):
     """Measured HBM rates of plain torch kernels on 4 GiB buffers, on the
     bench's stream: a fill (write only), a sum (read only) and a copy (read
@@ -234,26 +245,47 @@ def cpu_baseline(st, n_tokens, torch, W, PL):
     src_all = W.contiguous_src(w.T, w.G)
     chunk = 4096
     n_tokens = min(n_tokens, w.T)
-    total = 0.0
+    steps = {"stats": 0.0, "assign": 0.0, "dispatch": 0.0, "combine": 0.0}
     done = 0
-    for t0 in range(0, n_tokens, chunk):
-        n = min(chunk, n_tokens - t0)
-        topk = st.topk[t0:t0 + n].cpu().numpy()
-        gates = st.gates[t0:t0 + n].cpu().numpy()
-        src = np.ascontiguousarray(src_all[t0:t0 + n])
-        x = PL.bf16_bits(st.x[t0:t0 + n])
-        eo = PL.bf16_bits(st.eo[t0 * w.K:(t0 + n) * w.K])
-        c0 = time.perf_counter()
-        oracle.coact_stats(topk, w.E)
-        a, _ = oracle.assign(w.N, w.g, w.E, tabs, topk, src, seed=st.seed, step=0)
-        _, _, pos, _ = oracle.dispatch(a, w.G, src, x)
-        oracle.combine(eo, pos, gates)
-        total += time.perf_counter() - c0
-        done += n
+    # the oracle is single-threaded; the thread runs pinned to one host core
+    old_aff = os.sched_getaffinity(0)
+    core = min(old_aff)
+    os.sched_setaffinity(0, {core})
+    try:
+        for t0 in range(0, n_tokens, chunk):
+            n = min(chunk, n_tokens - t0)
+            topk = st.topk[t0:t0 + n].cpu().numpy()
+            gates = st.gates[t0:t0 + n].cpu().numpy()
+            src = np.ascontiguousarray(src_all[t0:t0 + n])
+            x = PL.bf16_bits(st.x[t0:t0 + n])
+            eo = PL.bf16_bits(st.eo[t0 * w.K:(t0 + n) * w.K])
+            c0 = time.perf_counter()
+            oracle.coact_stats(topk, w.E)
+            c1 = time.perf_counter()
+            a, _ = oracle.assign(w.N, w.g, w.E, tabs, topk, src, seed=st.seed, step=0)
+            c2 = time.perf_counter()
+            _, _, pos, _ = oracle.dispatch(a, w.G, src, x)
+            c3 = time.perf_counter()
+            oracle.combine(eo, pos, gates)
+            c4 = time.perf_counter()
+            for k, dt in zip(steps, (c1 - c0, c2 - c1, c3 - c2, c4 - c3)):
+                steps[k] += dt
+            done += n
+    finally:
+        os.sched_setaffinity(0, old_aff)
+    total = sum(steps.values())
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": done / total, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"first {done} tokens of the same workload in chunks of {chunk} "
                       f"(stats, assign, dispatch with packed rows, combine), "
-                      f"{total:.1f} s on one host core"}
+                      f"{total:.1f} s on one host core (core {core}, pinned)",
+            "seconds_per_step": {k: round(v, 3) for k, v in steps.items()},
+            "host_cpu": model, "host_cpus": os.cpu_count()}
 
 
 def main():
@@ -357,6 +389,11 @@ def main():
     if drift:
         wall = sum(e[0].elapsed_time(e[-1]) for e in evs) * 1e-3
 
+    step_ms = sorted(e[0].elapsed_time(e[-1]) for e in evs)
+
+    def pct(q):
+        return step_ms[min(len(step_ms) - 1, int(round(q * (len(step_ms) - 1))))]
+
     call_ms = {c: 0.0 for c in calls}
     for e in evs:
         for i, c in enumerate(calls):
@@ -397,6 +434,9 @@ def main():
                      "traffic": traffic},
         "pack_combine_hbm_frac": pc_bytes / pc_s / HBM_PEAK,
         "step_hbm_frac": step_bytes / (wall / args.steps) / HBM_PEAK,
+        "step_ms_percentiles": {"p10": pct(0.1), "median": pct(0.5), "p90": pct(0.9),
+                                "note": "per-step HIP events; value uses the wall clock"},
+        "device": device_info(torch),
         "call_ms": call_ms,
         "call_gbps": {c: ab[c] / (call_ms[c] * 1e-3) / 1e9 for c in calls},
     }
@@ -419,6 +459,11 @@ def main():
             V = sum(((rn32 >> n) & 1).sum().item() for n in range(w.N))
             per_rank = torch.bincount(st.assigned.flatten().long(), minlength=w.G).float()
             per_step.append((int(V), float(per_rank.max() / per_rank.mean())))
+        cycle_ms = [0.0] * w.steps
+        for k, e in enumerate(evs):
+            cycle_ms[k % w.steps] += e[0].elapsed_time(e[-1]) / sum(
+                1 for kk in range(args.steps) if kk % w.steps == k % w.steps)
+        result["cycle_step_ms"] = [round(v, 4) for v in cycle_ms]
         before, after = per_step[:w.swap_step], per_step[w.swap_step:]
         result["replan"] = {"method": "stage1_planner" if planner else "hot_order_recipe",
                             "before_step": w.swap_step,

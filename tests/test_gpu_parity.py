@@ -301,3 +301,18 @@ def test_replica_load_many_bands():
     B.cobalt_replica_load(dev_i32(topk), dev_i32(a), E, G, load,
                           B.replica_load_workspace_for(T, K, E, G))
     assert np.array_equal(u32(load), oracle.replica_load(topk, a, E, G))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("name,T,d", [("tiny", 4096, 512), ("clusters-e64", 32 * 97, 256),
+                                      ("colocate-e256", 64 * 30, 512), ("drift-e384", 64 * 21, 256)])
+def test_path_matches_oracle_over_seeds(seed, name, T, d):
+    """Every step at seeds 0, 1 and 2 (routing, layout and draws all change
+    with the seed), in both assignment modes."""
+    w = W.with_sizes(W.WORKLOADS[name], T=T, d=d)
+    print(f"seed case {name} seed={seed}", flush=True)
+    topk, gates = W.routing(w, seed)
+    table, owner = W.layout(w, seed)
+    for mode in (0, 1):
+        check_against_oracle(w, seed, topk.numpy(), gates.numpy(), table, owner, step=seed,
+                             mode=mode)
