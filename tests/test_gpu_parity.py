@@ -206,6 +206,9 @@ def _custom(N, g, E, S, K, T, d, seed, extra_per_rank=None):
     (4, 8, 64, 3, 1, 32 * 50, 8),       # K = 1 and one-vector rows
     (2, 4, 16, 4, 16, 8 * 90, 8200),    # K = 16; rows of 1025 vectors (long copy path)
     (8, 1, 8, 3, 4, 8 * 100, 16),       # one GPU per node
+    (2, 4, 16, 4, 4, 8 * 16, 16392),    # 17 slices of 2 KiB: the fan-out pack and
+                                        # one-wave-per-token combine
+    (2, 4, 16, 4, 8, 8 * 16, 16384),    # 16 slices: the largest scatter / fold shape
 ])
 def test_edge_shapes(N, g, E, S, K, T, d):
     w, topk, gates, table, owner = _custom(N, g, E, S, K, T, d, seed=N * 100 + K)
