@@ -209,6 +209,8 @@ def _custom(N, g, E, S, K, T, d, seed, extra_per_rank=None):
     (2, 4, 16, 4, 4, 8 * 16, 16392),    # 17 slices of 2 KiB: the fan-out pack and
                                         # one-wave-per-token combine
     (2, 4, 16, 4, 8, 8 * 16, 16384),    # 16 slices: the largest scatter / fold shape
+    (16, 8, 1024, 12, 8, 128 * 24, 64),  # E = 1024, G = 128: row-band statistics
+    (16, 32, 4096, 12, 8, 512 * 6, 16),  # E = 4096, G = 512: the largest tables
 ])
 def test_edge_shapes(N, g, E, S, K, T, d):
     w, topk, gates, table, owner = _custom(N, g, E, S, K, T, d, seed=N * 100 + K)
