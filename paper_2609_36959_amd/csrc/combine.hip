@@ -4,21 +4,26 @@
 // order; slots whose row is outside [0, T*K) are skipped.
 //
 // fold_kernel: one workgroup per (token, 2 KiB column slice), one wave per
-// slot j. Wave j loads its row's slice (non-temporal, two 16-byte chunks
-// per lane) into LDS; after a barrier wave 0 folds the K slices in slot
-// order and stores the slice of y. Each wave has a single row to fetch, so
-// many independent row loads are in flight; on the T=131072, K=8, d=7168
-// workload this runs at 6.1 TB/s, against 5.6 TB/s for combine_kernel.
+// slot j (at least four waves). Wave j loads its row's slice (non-temporal,
+// two 16-byte chunks per lane) into LDS; after a barrier four waves fold the
+// K slices in slot order, two 32-bit words per thread, and store the slice
+// of y. Each wave has a single row to fetch, so many independent row loads
+// are in flight; on the T=131072, K=8, d=7168 workload this runs at
+// 6.1-6.2 TB/s, against 5.6 TB/s for combine_kernel. Folding with one wave
+// (two chunks per lane) instead holds the stage longer and costs 2 %.
 //
 // combine_kernel (other shapes): each wave takes one (token, 1 KiB slice)
 // and loads the chunks of all K rows itself, issuing every load before its
 // single store so that no load waits behind a store.
+#include <algorithm>
+
 #include "internal.hpp"
 
 namespace cobalt {
 namespace {
 
 constexpr int kCombineWaves = 16;
+constexpr int kFoldWaves = 4;  // waves that fold a slice (128 chunks = 256 threads x 2 words)
 
 __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
     const uint32_t u = __float_as_uint(f);
@@ -93,8 +98,8 @@ __global__ __launch_bounds__(kMaxK * 64) void fold_kernel(
     const u32x4* __restrict__ eo, const int32_t* __restrict__ pos, const float* __restrict__ gates,
     int K, int64_t nch, int64_t TK, u32x4* __restrict__ y, float* __restrict__ y32) {
     // K slices of 128 chunks (K * 2 KiB, sized at launch): a small stage
-    // lets further workgroups start on a CU once the K - 1 loading waves of
-    // a workgroup have exited, which the wave count alone would not limit
+    // lets further workgroups start on a CU once the loading waves of a
+    // workgroup have exited, which the wave count alone would not limit
     extern __shared__ u32x4 stage[];
     __shared__ float gate[kMaxK];
     __shared__ int valid[kMaxK];
@@ -105,48 +110,49 @@ __global__ __launch_bounds__(kMaxK * 64) void fold_kernel(
     const int lane = threadIdx.x & 63;
     const int64_t c0 = (int64_t)g * 128 + lane;
     const bool in0 = c0 < nch, in1 = c0 + 64 < nch;
-    const int p = pos[(int64_t)t * K + j];
-    const bool ok = p >= 0 && p < TK;
-    if (ok) {
-        const u32x4* row = eo + (int64_t)p * nch;
-        if (in0) stage[j * 128 + lane] = __builtin_nontemporal_load(row + c0);
-        if (in1) stage[j * 128 + lane + 64] = __builtin_nontemporal_load(row + c0 + 64);
-    }
-    const float gj = gates[(int64_t)t * K + j];
-    if (lane == 0) {
-        valid[j] = ok;
-        gate[j] = gj;
+    if (j < K) {
+        const int p = pos[(int64_t)t * K + j];
+        const bool ok = p >= 0 && p < TK;
+        // both loads are issued before either LDS write: a write right after
+        // its own load would make the second load wait for the first
+        const u32x4* row = eo + (int64_t)(ok ? p : 0) * nch;
+        u32x4 v0, v1;
+        if (ok && in0) v0 = __builtin_nontemporal_load(row + c0);
+        if (ok && in1) v1 = __builtin_nontemporal_load(row + c0 + 64);
+        if (ok && in0) stage[j * 128 + lane] = v0;
+        if (ok && in1) stage[j * 128 + lane + 64] = v1;
+        const float gj = gates[(int64_t)t * K + j];
+        if (lane == 0) {
+            valid[j] = ok;
+            gate[j] = gj;
+        }
     }
     __syncthreads();
-    if (j != 0) return;
+    // kFoldWaves waves fold: thread i takes words 2i, 2i+1 of the slice
+    // (four bf16 values of chunk i / 2), summing the K slots in slot order
+    if (j >= kFoldWaves) return;
+    const int i = threadIdx.x;
+    const int64_t c = (int64_t)g * 128 + (i >> 1);
+    if (c >= nch) return;
+    const uint32_t* s32 = (const uint32_t*)stage;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < K; ++k) {
+        if (!valid[k]) continue;
+        const float gk = gate[k];
+        const u32x2 v = *(const u32x2*)(s32 + k * 512 + 2 * i);
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const int64_t c = c0 + 64 * h;
-        if (c >= nch) break;
-        float acc[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) acc[q] = 0.f;
-        for (int k = 0; k < K; ++k) {
-            if (!valid[k]) continue;
-            const float gk = gate[k];
-            const u32x4 v = stage[k * 128 + lane + 64 * h];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                acc[2 * q] = __builtin_fmaf(gk, __uint_as_float(v[q] << 16), acc[2 * q]);
-                acc[2 * q + 1] = __builtin_fmaf(gk, __uint_as_float(v[q] & 0xffff0000u), acc[2 * q + 1]);
-            }
-        }
-        u32x4 out;
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-            out[q] = f32_to_bf16_rne(acc[2 * q]) | (f32_to_bf16_rne(acc[2 * q + 1]) << 16);
-        __builtin_nontemporal_store(out, y + (int64_t)t * nch + c);
-        if (kF32) {
-            float4* o = (float4*)(y32 + ((int64_t)t * nch + c) * 8);
-            o[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-            o[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+        for (int q = 0; q < 2; ++q) {
+            acc[2 * q] = __builtin_fmaf(gk, __uint_as_float(v[q] << 16), acc[2 * q]);
+            acc[2 * q + 1] = __builtin_fmaf(gk, __uint_as_float(v[q] & 0xffff0000u), acc[2 * q + 1]);
         }
     }
+    u32x2 out;
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+        out[q] = f32_to_bf16_rne(acc[2 * q]) | (f32_to_bf16_rne(acc[2 * q + 1]) << 16);
+    const int64_t w = ((int64_t)t * nch + (int64_t)g * 128) * 4 + 2 * i;  // word index in y
+    __builtin_nontemporal_store(out, (u32x2*)((uint32_t*)y + w));
+    if (kF32) *(float4*)(y32 + 2 * w) = make_float4(acc[0], acc[1], acc[2], acc[3]);
 }
 
 template <bool kF32, int GROUPS>
@@ -154,7 +160,8 @@ bool try_fold(const void* eo, const int32_t* pos, const float* gates, int64_t T,
               int64_t nch, void* y, float* y32, hipStream_t s) {
     if ((nch + 127) / 128 != GROUPS) return try_fold<kF32, GROUPS - 1>(eo, pos, gates, T, K, nch, y, y32, s);
     if (T * GROUPS >= (int64_t(1) << 31)) return false;
-    hipLaunchKernelGGL((fold_kernel<kF32, GROUPS>), dim3((unsigned)(T * GROUPS)), dim3(K * 64),
+    hipLaunchKernelGGL((fold_kernel<kF32, GROUPS>), dim3((unsigned)(T * GROUPS)),
+                       dim3(std::max(K, kFoldWaves) * 64),
                        (size_t)K * 128 * sizeof(u32x4), s,
                        (const u32x4*)eo, pos, gates, K, nch, T * K, (u32x4*)y, y32);
     return true;

@@ -534,7 +534,9 @@ __global__ __launch_bounds__(kMaxK * 64) void scatter_kernel(
     const int64_t c0 = (int64_t)g * 128 + (threadIdx.x & 63);
     // The x loads are issued before the packed row is read: a branch on the
     // row first would make every wave wait for that load before its own
-    // two loads start (measured: 3.45 ms instead of 2.95 ms).
+    // two loads start (measured: 3.45 ms instead of 2.95 ms). The in-range
+    // guards also keep them there: without them the compiler sinks both
+    // loads below the branch on p, with the same cost (3.42 ms at d = 7168).
     const u32x4* row = x + (int64_t)t * nch;
     const bool in0 = c0 < nch, in1 = c0 + 64 < nch;
     u32x4 v0, v1;
