@@ -66,6 +66,7 @@ def lib():
         L.ref_dispatch.argtypes = [P, P, i64, i32, i32, P, i64, P, P, P, P]
         L.ref_node_dispatch.argtypes = [P, P, i64, i32, i32, i32, P, i64, P, P, P, P, P, P]
         L.ref_combine.argtypes = [P, i64, P, P, i64, i32, i64, P, P]
+        L.ref_node_combine.argtypes = [P, i64, P, P, P, P, i64, i32, i32, i32, i64, i64, P, P]
         L.ref_traffic.argtypes = [P, P, i64, i32, i32, i32, P, P, P]
         L.ref_count_ema.argtypes = [P, i64, ctypes.c_float, i32, i32, P]
         L.ref_ochiai.argtypes = [P, P, i32, P]
@@ -224,6 +225,29 @@ def combine(expert_out, pos, gates):
     _check(lib().ref_combine(_p(eo), rows, _p(pos), _p(gates), T, K, d, _p(y), _p(y32)),
            "combine")
     return y, y32
+
+
+def node_combine(expert_out, pos, assigned, gates, node_pos, g, node_rows=None):
+    """Node-level combine. expert_out: uint16 bf16 bits [rows, d]; pos,
+    assigned, gates [T, K]; node_pos [T, N]; node_rows defaults to the
+    largest row node_pos names plus one. Returns (partial bf16 bits
+    [node_rows, d] u16, rows no entry of node_pos names left zero; y bf16
+    bits [T, d] u16)."""
+    eo = _c(expert_out, np.uint16)
+    rows, d = eo.shape
+    pos = _c(pos, np.int32)
+    assigned = _c(assigned, np.int32)
+    gates = _c(gates, np.float32)
+    node_pos = _c(node_pos, np.int32)
+    T, K = pos.shape
+    N = node_pos.shape[1]
+    if node_rows is None:
+        node_rows = int(node_pos.max()) + 1 if node_pos.size else 0
+    partial = np.zeros((max(node_rows, 1), d), np.uint16)
+    y = np.zeros((T, d), np.uint16)
+    _check(lib().ref_node_combine(_p(eo), rows, _p(pos), _p(assigned), _p(gates), _p(node_pos),
+                                  T, K, N, g, d, node_rows, _p(partial), _p(y)), "node_combine")
+    return partial[:node_rows], y
 
 
 def traffic(assigned, N, g, src=None):

@@ -451,6 +451,60 @@ int ref_combine(const uint16_t* expert_out, int64_t rows, const int32_t* pos, co
 }
 
 /* ---------------------------------------------------------------------- */
+/* Node-level combine, the reverse of the node-deduplicated dispatch      */
+/* (Section 1 and Section 3.1: a token's results leave a node once). On    */
+/* node n the slots of token t whose rank r_tj lies on n (r_tj / g = n)   */
+/* are summed first, fp32 from 0, one fused multiply-add per slot in slot */
+/* order, and the partial is rounded to bf16:                             */
+/*   part[t][n][c] = bf16( sum_{j on n} gates[t][j] * eo[pos[t][j]][c] )  */
+/* It is stored in row node_pos[t][n] of partial, the row the dispatch     */
+/* used for (t, n). At the source the partials are summed, fp32 from 0,    */
+/* in increasing n, and rounded once more:                                */
+/*   y[t][c] = bf16( sum_{n : node_pos[t][n] valid} float(part[t][n][c]) ) */
+/* Skipped: slots with a rank outside [0, N*g) or a row outside [0, rows); */
+/* node rows outside [0, node_rows) (neither written nor summed). A valid  */
+/* node row with no slot of its token on the node holds zero.             */
+/* ---------------------------------------------------------------------- */
+int ref_node_combine(const uint16_t* expert_out, int64_t rows, const int32_t* pos,
+                     const int32_t* assigned, const float* gates, const int32_t* node_pos,
+                     int64_t T, int32_t K, int32_t N, int32_t g, int64_t d, int64_t node_rows,
+                     uint16_t* partial, uint16_t* y)
+{
+    if (T < 0 || K < 1 || N < 1 || N > 32 || g < 1 || g > 32 || d < 0 || node_rows < 0)
+        return REF_EINVAL;
+    int32_t G = N * g;
+    /* node side: one partial row per (token, node) */
+    for (int64_t t = 0; t < T; ++t)
+        for (int32_t n = 0; n < N; ++n) {
+            int64_t nrow = node_pos[t * N + n];
+            if (nrow < 0 || nrow >= node_rows) continue;
+            for (int64_t c = 0; c < d; ++c) {
+                float acc = 0.0f;
+                for (int32_t j = 0; j < K; ++j) {
+                    int32_t r = assigned[t * K + j];
+                    int64_t row = pos[t * K + j];
+                    if (r < 0 || r >= G || r / g != n) continue;
+                    if (row < 0 || row >= rows) continue;
+                    acc = fmaf(gates[t * K + j], ref_bf16_to_f32(expert_out[row * d + c]), acc);
+                }
+                partial[nrow * d + c] = ref_f32_to_bf16(acc);
+            }
+        }
+    /* source side: the partials of each token, in increasing n */
+    for (int64_t t = 0; t < T; ++t)
+        for (int64_t c = 0; c < d; ++c) {
+            float acc = 0.0f;
+            for (int32_t n = 0; n < N; ++n) {
+                int64_t nrow = node_pos[t * N + n];
+                if (nrow < 0 || nrow >= node_rows) continue;
+                acc = acc + ref_bf16_to_f32(partial[nrow * d + c]);
+            }
+            y[t * d + c] = ref_f32_to_bf16(acc);
+        }
+    return REF_OK;
+}
+
+/* ---------------------------------------------------------------------- */
 /* Traffic model (Eq. 1) and load: V = sum over tokens of the number of    */
 /* distinct nodes other than node(s_t) among the token's assigned ranks;   */
 /* cross_pairs counts pairs whose rank is on another node; load[r] counts  */

@@ -49,6 +49,21 @@ MUTANTS = [
     ("forwarding mask uses global rank bits", "                mask[r / g] |= 1u << (r % g);\n            }\n            for (int32_t n = 0; n < N; ++n) {\n                if (!mask[n]) {",
      "                mask[r / g] |= 1u << (r % 32);\n            }\n            for (int32_t n = 0; n < N; ++n) {\n                if (!mask[n]) {",
      ["test_oracle_node_dispatch.py"]),
+    ("node combine sums the partials in decreasing node order",
+     "            for (int32_t n = 0; n < N; ++n) {\n                int64_t nrow = node_pos[t * N + n];\n                if (nrow < 0 || nrow >= node_rows) continue;\n                acc = acc + ",
+     "            for (int32_t n = N - 1; n >= 0; --n) {\n                int64_t nrow = node_pos[t * N + n];\n                if (nrow < 0 || nrow >= node_rows) continue;\n                acc = acc + ",
+     ["test_oracle_node_combine.py"]),
+    ("node combine takes the node of a rank as r % g",
+     "if (r < 0 || r >= G || r / g != n) continue;", "if (r < 0 || r >= G || r % g != n) continue;",
+     ["test_oracle_node_combine.py"]),
+    ("node combine drops the gate",
+     "acc = fmaf(gates[t * K + j], ref_bf16_to_f32(expert_out[row * d + c]), acc);\n                }\n                partial[",
+     "acc = acc + ref_bf16_to_f32(expert_out[row * d + c]);\n                }\n                partial[",
+     ["test_oracle_node_combine.py"]),
+    ("node combine truncates the partials",
+     "partial[nrow * d + c] = ref_f32_to_bf16(acc);",
+     "{ union { float f; uint32_t u; } cv; cv.f = acc; partial[nrow * d + c] = (uint16_t)(cv.u >> 16); }",
+     ["test_oracle_node_combine.py"]),
     ("EMA weights swapped", "ema[i] = fmaf(decay, ema[i], gain * x);",
      "ema[i] = fmaf(gain, ema[i], decay * x);", ["test_oracle_ema.py"]),
     ("Ochiai diagonal left at zero", "uint32_t c = i == j ? count[i] : coact[(int64_t)i * E + j];",
