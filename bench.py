@@ -30,7 +30,7 @@ HBM_PEAK = 8.0e12  # MI355X HBM3E, bytes/s
 METRIC = "routed tokens/sec (stats+assign+pack+combine), % of HBM peak, 1 MI355X"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_{call}_{workload}.txt")
 KERNEL_SOURCES = {"cobalt_dispatch_pack": "dispatch.hip", "cobalt_combine": "combine.hip",
-                  "cobalt_node_dispatch_pack": "dispatch.hip"}
+                  "cobalt_node_dispatch_pack": "dispatch.hip", "cobalt_node_combine": "combine.hip"}
 
 
 def parse():
@@ -70,6 +70,15 @@ def node_dispatch_bytes(w, rows):
     forwarding masks and row tokens, and the [G][N] counts and offsets."""
     T, K, d, N, G = w.T, w.K, w.d, w.N, w.G
     return T * K * 4 + T * d * 2 + rows * d * 2 + T * N * 4 + rows * 8 + 12 * G * N
+
+
+def node_combine_bytes(w, rows):
+    """Bytes the node-level combine must move: the node side reads every
+    pair's expert row, its pos, rank and gate and the node rows, and writes
+    `rows` bf16 partials; the source side reads the partials and node_pos
+    and writes y."""
+    T, K, d, N = w.T, w.K, w.d, w.N
+    return T * K * d * 2 + T * K * 12 + 2 * T * N * 4 + 2 * rows * d * 2 + T * d * 2
 
 
 def source_digest(call):
@@ -532,6 +541,22 @@ def main():
         "hbm_frac": nb / (node_ms * 1e-3) / HBM_PEAK,
         "traffic": measured_traffic("cobalt_node_dispatch_pack", wl_name),
         "pair_pack_ms": call_ms["cobalt_dispatch_pack"], "node_pack_ms": node_ms}
+    # its reverse: per-(token, node) partial sums, then the source-side sum
+    with torch.cuda.stream(stream):
+        st.node_combine(stream=stream)
+        ev[0].record(stream)
+        for _ in range(args.steps):
+            st.node_combine(stream=stream)
+        ev[1].record(stream)
+    torch.cuda.synchronize()
+    ncb_ms = ev[0].elapsed_time(ev[1]) / args.steps
+    cb = node_combine_bytes(w, rows)
+    result["extra_calls_ms"]["cobalt_node_combine"] = ncb_ms
+    result["node_dedup_combine"] = {
+        "algorithmic_bytes": cb, "achieved_gbps": cb / (ncb_ms * 1e-3) / 1e9,
+        "hbm_frac": cb / (ncb_ms * 1e-3) / HBM_PEAK, "node_combine_ms": ncb_ms,
+        "pair_combine_ms": call_ms["cobalt_combine"],
+        "cross_node_rows": rows - local_rows}
     # planner statistics of one step: EMA update of the co-activation and
     # expert counts, and the Ochiai similarity (the Fig. 3 statistic)
     st.coact.zero_()

@@ -199,6 +199,39 @@ cobalt_status cobalt_node_dispatch_pack(const int32_t* assigned_rank, const int3
                                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Step 4': node-level combine, the reverse of the node-deduplicated
+ * dispatch (Section 1 and Section 3.1: a token's results leave a node once,
+ * so the combine's cross-node rows also number Eq. 1's V).
+ *
+ * On node n the slots of token t whose rank lies on n are summed first:
+ *   part[t][n][c] = bf16_rne( sum_{j : r_tj / gpus_per_node = n}
+ *                             gates[t][j] * expert_out[pos[t][j]][c] ),
+ * in fp32 from 0 with one fused multiply-add per slot in slot order. The
+ * partial is stored as bf16, like the rows of the dispatch, in row
+ * node_pos[t][n] of node_partial, the row the node-deduplicated dispatch
+ * used for (t, n). At the source the partials are summed in increasing n:
+ *   y[t][c] = bf16_rne( sum_{n : node_pos[t][n] >= 0} float(part[t][n][c]) ),
+ * in fp32 from 0.
+ * expert_out [T*K][d] bf16 in, in the per-pair packed layout; pos [T][K]
+ *   int32 in (from cobalt_dispatch_pack); assigned_rank [T][K] int32 in;
+ *   gates [T][K] fp32 in; node_pos [T][N] int32 in (from
+ *   cobalt_node_dispatch_pack on the same assigned_rank and src_rank).
+ * node_partial [T*min(K,N)][d] bf16 out: only the rows that node_pos names
+ *   are written. y [T][d] bf16 out.
+ * G = N * gpus_per_node. A slot is skipped if its rank is outside [0, G)
+ *   or its row outside [0, T*K); a node_pos entry outside
+ *   [0, T*min(K,N)) is neither written nor summed. A named node row with
+ *   no slot of its token on the node is written as zero.
+ * The result differs from cobalt_combine by the rounding of the partials
+ *   to bf16 (with a single node it is identical).
+ * ---------------------------------------------------------------------- */
+cobalt_status cobalt_node_combine(const void* expert_out, const int32_t* pos,
+                                  const int32_t* assigned_rank, const float* gates,
+                                  const int32_t* node_pos, int64_t T, int32_t K, int32_t N,
+                                  int32_t gpus_per_node, int64_t d, void* node_partial, void* y,
+                                  void* stream);
+
+/* ------------------------------------------------------------------------
  * Step 4: combine and weighted sum (Fig. 1, last stage).
  *
  * expert_out [T*K][d] bf16 in, in the packed layout (row pos[p] holds the

@@ -63,6 +63,7 @@ def lib() -> ctypes.CDLL:
         "cobalt_node_dispatch_pack": ([P, P, i64, i32, i32, i32, P, i64, P, P, P, P, P, P, P, sz,
                                        P], ctypes.c_int),
         "cobalt_combine": ([P, P, P, i64, i32, i64, P, P, P], ctypes.c_int),
+        "cobalt_node_combine": ([P, P, P, P, P, i64, i32, i32, i32, i64, P, P, P], ctypes.c_int),
         "cobalt_coact_ema": ([P, P, i32, ctypes.c_float, i32, P, P, P, P], ctypes.c_int),
         "cobalt_count_ema": ([P, i64, ctypes.c_float, i32, P, P], ctypes.c_int),
         "cobalt_validate_routing": ([P, P, i64, i32, i32, i32, P, P], ctypes.c_int),
@@ -262,6 +263,20 @@ def cobalt_combine(expert_out: torch.Tensor, pos: torch.Tensor, gates: torch.Ten
     _call("cobalt_combine", _dev(expert_out, "expert_out", BF16, (T * K, d)),
           _dev(pos, "pos", I32), _dev(gates, "gates", F32, (T, K)), T, K, d,
           _dev(y, "y", BF16, (T, d)), _dev(y_f32, "y_f32", F32, (T, d)), _stream(stream))
+
+
+def cobalt_node_combine(expert_out: torch.Tensor, pos: torch.Tensor, assigned_rank: torch.Tensor,
+                        gates: torch.Tensor, node_pos: torch.Tensor, N: int, gpus_per_node: int,
+                        node_partial: torch.Tensor, y: torch.Tensor, stream=None) -> None:
+    """node_partial holds T * min(K, N) rows; node_pos comes from
+    cobalt_node_dispatch_pack on the same assigned ranks."""
+    T, K = pos.shape
+    d = y.shape[1]
+    _call("cobalt_node_combine", _dev(expert_out, "expert_out", BF16, (T * K, d)),
+          _dev(pos, "pos", I32, (T, K)), _dev(assigned_rank, "assigned_rank", I32, (T, K)),
+          _dev(gates, "gates", F32, (T, K)), _dev(node_pos, "node_pos", I32, (T, N)), T, K, N,
+          gpus_per_node, d, _dev(node_partial, "node_partial", BF16, (T * min(K, N), d)),
+          _dev(y, "y", BF16, (T, d)), _stream(stream))
 
 
 def cobalt_replica_load_workspace_bytes(T: int, K: int, E: int, G: int) -> int:

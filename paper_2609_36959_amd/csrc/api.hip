@@ -282,6 +282,23 @@ extern "C" cobalt_status cobalt_combine(const void* eo, const int32_t* pos, cons
     return launch_combine(eo, pos, gates, T, K, d, y, y32, (hipStream_t)stream);
 }
 
+extern "C" cobalt_status cobalt_node_combine(const void* eo, const int32_t* pos,
+                                             const int32_t* assigned, const float* gates,
+                                             const int32_t* node_pos, int64_t T, int32_t K,
+                                             int32_t N, int32_t gpn, int64_t d, void* partial,
+                                             void* y, void* stream) {
+    if (T < 0 || K < 1 || K > kMaxK || N < 1 || N > kMaxN || gpn < 1 || gpn > kMaxGpn || d < 8 ||
+        d % 8 != 0)
+        return COBALT_EINVAL;  // N * gpn <= kMaxN * kMaxGpn = kMaxG
+    if (T > 0 && (!eo || !pos || !assigned || !gates || !node_pos || !partial || !y))
+        return COBALT_EINVAL;
+    if (T > 0 && (!aligned16(eo) || !aligned16(partial) || !aligned16(y))) return COBALT_EINVAL;
+    if (T * K >= (int64_t(1) << 31)) return COBALT_EUNSUPPORTED;
+    if (T == 0) return COBALT_OK;
+    return launch_node_combine(eo, pos, assigned, gates, node_pos, T, K, N, gpn, d, partial, y,
+                               (hipStream_t)stream);
+}
+
 extern "C" size_t cobalt_replica_load_workspace_bytes(int64_t T, int32_t K, int32_t E,
                                                      int32_t G) {
     if (T < 0 || K < 1 || K > kMaxK || E < 1 || E > kMaxE || G < 1 || G > kMaxG) return 0;

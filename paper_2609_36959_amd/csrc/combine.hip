@@ -92,20 +92,25 @@ __global__ __launch_bounds__(kCombineWaves * 64) void combine_kernel(
 }
 
 // GROUPS = slices of 128 chunks per row, a template parameter so that the
-// block index splits into (token, slice) with a constant division.
-template <bool kF32, int GROUPS>
+// block index splits into (token, slice) with a constant division; 0 takes
+// the count from groups_rt (rows wider than 16 slices). kUnit: every gate
+// is 1 and gates is not read (the source-side sum of the node-level
+// combine; fma(1, v, acc) rounds exactly as acc + v).
+template <bool kF32, int GROUPS, bool kUnit>
 __global__ __launch_bounds__(kMaxK * 64) void fold_kernel(
     const u32x4* __restrict__ eo, const int32_t* __restrict__ pos, const float* __restrict__ gates,
-    int K, int64_t nch, int64_t TK, u32x4* __restrict__ y, float* __restrict__ y32) {
+    int K, int64_t nch, int64_t TK, int groups_rt, u32x4* __restrict__ y,
+    float* __restrict__ y32) {
     // K slices of 128 chunks (K * 2 KiB, sized at launch): a small stage
     // lets further workgroups start on a CU once the loading waves of a
     // workgroup have exited, which the wave count alone would not limit
     extern __shared__ u32x4 stage[];
     __shared__ float gate[kMaxK];
     __shared__ int valid[kMaxK];
+    const uint32_t groups = GROUPS ? GROUPS : (uint32_t)groups_rt;
     const uint32_t tg = blockIdx.x;
-    const uint32_t t = tg / GROUPS;
-    const uint32_t g = tg - t * GROUPS;
+    const uint32_t t = tg / groups;
+    const uint32_t g = tg - t * groups;
     const int j = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int64_t c0 = (int64_t)g * 128 + lane;
@@ -121,7 +126,7 @@ __global__ __launch_bounds__(kMaxK * 64) void fold_kernel(
         if (ok && in1) v1 = __builtin_nontemporal_load(row + c0 + 64);
         if (ok && in0) stage[j * 128 + lane] = v0;
         if (ok && in1) stage[j * 128 + lane + 64] = v1;
-        const float gj = gates[(int64_t)t * K + j];
+        const float gj = kUnit ? 1.0f : gates[(int64_t)t * K + j];
         if (lane == 0) {
             valid[j] = ok;
             gate[j] = gj;
@@ -155,26 +160,112 @@ __global__ __launch_bounds__(kMaxK * 64) void fold_kernel(
     if (kF32) *(float4*)(y32 + 2 * w) = make_float4(acc[0], acc[1], acc[2], acc[3]);
 }
 
-template <bool kF32, int GROUPS>
+template <bool kF32, int GROUPS, bool kUnit>
 bool try_fold(const void* eo, const int32_t* pos, const float* gates, int64_t T, int K,
-              int64_t nch, void* y, float* y32, hipStream_t s) {
-    if ((nch + 127) / 128 != GROUPS) return try_fold<kF32, GROUPS - 1>(eo, pos, gates, T, K, nch, y, y32, s);
-    if (T * GROUPS >= (int64_t(1) << 31)) return false;
-    hipLaunchKernelGGL((fold_kernel<kF32, GROUPS>), dim3((unsigned)(T * GROUPS)),
+              int64_t nch, int64_t TK, void* y, float* y32, hipStream_t s) {
+    const int64_t groups = (nch + 127) / 128;
+    if constexpr (GROUPS > 0) {
+        if (groups != GROUPS)
+            return try_fold<kF32, GROUPS - 1, kUnit>(eo, pos, gates, T, K, nch, TK, y, y32, s);
+    } else if constexpr (!kUnit) {
+        return false;  // the plain combine has combine_kernel for wide rows
+    }
+    if (T * groups >= (int64_t(1) << 31)) return false;
+    hipLaunchKernelGGL((fold_kernel<kF32, GROUPS, kUnit>), dim3((unsigned)(T * groups)),
                        dim3(std::max(K, kFoldWaves) * 64),
                        (size_t)K * 128 * sizeof(u32x4), s,
-                       (const u32x4*)eo, pos, gates, K, nch, T * K, (u32x4*)y, y32);
+                       (const u32x4*)eo, pos, gates, K, nch, TK, (int)groups, (u32x4*)y, y32);
     return true;
 }
-template <>
-bool try_fold<false, 0>(const void*, const int32_t*, const float*, int64_t, int, int64_t, void*,
-                        float*, hipStream_t) {
-    return false;
+
+// Node side of the node-level combine: one workgroup per (token, 2 KiB
+// column slice), one wave per slot j (at least four waves). Wave j loads its
+// row's slice like fold_kernel and records its gate and its rank's node;
+// after a barrier four waves fold, for each node the token reaches, the
+// slots on that node in slot order (two 32-bit words per thread), and store
+// the bf16 partial in the token's row for that node. GROUPS as for
+// fold_kernel.
+template <int GROUPS>
+__global__ __launch_bounds__(kMaxK * 64) void node_fold_kernel(
+    const u32x4* __restrict__ eo, const int32_t* __restrict__ pos,
+    const int32_t* __restrict__ assigned, const float* __restrict__ gates,
+    const int32_t* __restrict__ node_pos, int K, int N, int gpn, int64_t nch, int64_t TK,
+    int64_t node_rows, int groups_rt, u32x4* __restrict__ partial) {
+    extern __shared__ u32x4 stage[];
+    __shared__ float gate[kMaxK];
+    __shared__ int slot_node[kMaxK];  // node of slot j's rank, -1 for a skipped slot
+    __shared__ int nrow[kMaxN];       // row of (t, n) in partial, -1 if none
+    const uint32_t groups = GROUPS ? GROUPS : (uint32_t)groups_rt;
+    const uint32_t tg = blockIdx.x;
+    const uint32_t t = tg / groups;
+    const uint32_t g = tg - t * groups;
+    const int j = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const int64_t c0 = (int64_t)g * 128 + lane;
+    const bool in0 = c0 < nch, in1 = c0 + 64 < nch;
+    if (j < K) {
+        const int p = pos[(int64_t)t * K + j];
+        const int r = assigned[(int64_t)t * K + j];
+        const bool ok = p >= 0 && p < TK && r >= 0 && r < N * gpn;
+        const u32x4* row = eo + (int64_t)(ok ? p : 0) * nch;
+        u32x4 v0, v1;
+        if (ok && in0) v0 = __builtin_nontemporal_load(row + c0);
+        if (ok && in1) v1 = __builtin_nontemporal_load(row + c0 + 64);
+        if (ok && in0) stage[j * 128 + lane] = v0;
+        if (ok && in1) stage[j * 128 + lane + 64] = v1;
+        const float gj = gates[(int64_t)t * K + j];
+        if (lane == 0) {
+            gate[j] = gj;
+            slot_node[j] = ok ? r / gpn : -1;
+        }
+    }
+    if (j == 0 && lane < N) {
+        const int q = node_pos[(int64_t)t * N + lane];
+        nrow[lane] = q >= 0 && q < node_rows ? q : -1;
+    }
+    __syncthreads();
+    if (j >= kFoldWaves) return;
+    const int i = threadIdx.x;
+    const int64_t c = (int64_t)g * 128 + (i >> 1);
+    if (c >= nch) return;
+    const uint32_t* s32 = (const uint32_t*)stage;
+    for (int n = 0; n < N; ++n) {
+        const int q = nrow[n];
+        if (q < 0) continue;
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int k = 0; k < K; ++k) {
+            if (slot_node[k] != n) continue;
+            const float gk = gate[k];
+            const u32x2 v = *(const u32x2*)(s32 + k * 512 + 2 * i);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                acc[2 * h] = __builtin_fmaf(gk, __uint_as_float(v[h] << 16), acc[2 * h]);
+                acc[2 * h + 1] = __builtin_fmaf(gk, __uint_as_float(v[h] & 0xffff0000u), acc[2 * h + 1]);
+            }
+        }
+        u32x2 out;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            out[h] = f32_to_bf16_rne(acc[2 * h]) | (f32_to_bf16_rne(acc[2 * h + 1]) << 16);
+        const int64_t w = ((int64_t)q * nch + (int64_t)g * 128) * 4 + 2 * i;
+        __builtin_nontemporal_store(out, (u32x2*)((uint32_t*)partial + w));
+    }
 }
-template <>
-bool try_fold<true, 0>(const void*, const int32_t*, const float*, int64_t, int, int64_t, void*,
-                       float*, hipStream_t) {
-    return false;
+
+template <int GROUPS>
+void launch_node_fold(const void* eo, const int32_t* pos, const int32_t* assigned,
+                      const float* gates, const int32_t* node_pos, int64_t T, int K, int N,
+                      int gpn, int64_t nch, int64_t node_rows, void* partial, hipStream_t s) {
+    const int64_t groups = (nch + 127) / 128;
+    if constexpr (GROUPS > 0) {
+        if (groups != GROUPS)
+            return launch_node_fold<GROUPS - 1>(eo, pos, assigned, gates, node_pos, T, K, N, gpn,
+                                                nch, node_rows, partial, s);
+    }
+    hipLaunchKernelGGL(node_fold_kernel<GROUPS>, dim3((unsigned)(T * groups)),
+                       dim3(std::max(K, kFoldWaves) * 64), (size_t)K * 128 * sizeof(u32x4), s,
+                       (const u32x4*)eo, pos, assigned, gates, node_pos, K, N, gpn, nch, T * K,
+                       node_rows, (int)groups, (u32x4*)partial);
 }
 
 }  // namespace
@@ -182,8 +273,8 @@ bool try_fold<true, 0>(const void*, const int32_t*, const float*, int64_t, int, 
 cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* gates, int64_t T,
                              int K, int64_t d, void* y, float* y32, hipStream_t s) {
     const int64_t nch = d / 8;
-    if (y32 ? try_fold<true, 16>(eo, pos, gates, T, K, nch, y, y32, s)
-            : try_fold<false, 16>(eo, pos, gates, T, K, nch, y, y32, s)) {
+    if (y32 ? try_fold<true, 16, false>(eo, pos, gates, T, K, nch, T * K, y, y32, s)
+            : try_fold<false, 16, false>(eo, pos, gates, T, K, nch, T * K, y, y32, s)) {
         COBALT_LAUNCH_CHECK();
         return COBALT_OK;
     }
@@ -197,6 +288,23 @@ cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* ga
         y32 ? launch(combine_kernel<true, 8>) : launch(combine_kernel<false, 8>);
     else
         y32 ? launch(combine_kernel<true, 0>) : launch(combine_kernel<false, 0>);
+    COBALT_LAUNCH_CHECK();
+    return COBALT_OK;
+}
+
+cobalt_status launch_node_combine(const void* eo, const int32_t* pos, const int32_t* assigned,
+                                  const float* gates, const int32_t* node_pos, int64_t T, int K,
+                                  int N, int gpn, int64_t d, void* partial, void* y,
+                                  hipStream_t s) {
+    const int64_t nch = d / 8;
+    const int64_t groups = (nch + 127) / 128;
+    if (T * groups >= (int64_t(1) << 31)) return COBALT_EUNSUPPORTED;
+    const int64_t node_rows = T * std::min(K, N);
+    launch_node_fold<16>(eo, pos, assigned, gates, node_pos, T, K, N, gpn, nch, node_rows,
+                         partial, s);
+    COBALT_LAUNCH_CHECK();
+    // source side: y[t] = sum over n of partial[node_pos[t][n]], n increasing
+    try_fold<false, 16, true>(partial, node_pos, nullptr, T, N, nch, node_rows, y, nullptr, s);
     COBALT_LAUNCH_CHECK();
     return COBALT_OK;
 }

@@ -13,6 +13,7 @@ namespace cobalt {
 constexpr int kMaxN = 16;
 constexpr int kMaxGpn = 32;
 constexpr int kMaxG = 512;
+static_assert(kMaxN * kMaxGpn <= kMaxG, "N and gpus_per_node in range bound G");
 constexpr int kMaxK = 16;
 constexpr int kMaxE = 4096;
 
@@ -60,6 +61,10 @@ cobalt_status launch_node_dispatch(const int32_t* assigned, const int32_t* src, 
                                    int32_t* row_token, void* packed, void* ws, hipStream_t s);
 cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* gates, int64_t T,
                              int K, int64_t d, void* y, float* y32, hipStream_t s);
+cobalt_status launch_node_combine(const void* eo, const int32_t* pos, const int32_t* assigned,
+                                  const float* gates, const int32_t* node_pos, int64_t T, int K,
+                                  int N, int gpn, int64_t d, void* partial, void* y,
+                                  hipStream_t s);
 size_t replica_load_workspace_bytes(int64_t T, int K, int E, int G);
 cobalt_status launch_replica_load(const int32_t* topk, const int32_t* assigned, int64_t T, int K,
                                   int E, int G, uint32_t* load, void* ws, size_t ws_bytes,

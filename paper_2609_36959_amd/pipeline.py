@@ -109,6 +109,18 @@ class RoutingStep:
                                     self.row_token, self.node_packed, self.node_workspace,
                                     stream=stream)
 
+    def node_combine(self, stream=None):
+        """Node-level combine of the expert outputs over the node rows of the
+        last node_pack: bf16 partials per (token, node) in node_partial, then
+        y_node; buffers are allocated on first use."""
+        w = self.w
+        if getattr(self, "node_partial", None) is None:
+            cap = w.T * min(w.K, w.N)
+            self.node_partial = torch.empty(cap, w.d, dtype=torch.bfloat16, device=self.device)
+            self.y_node = torch.empty(w.T, w.d, dtype=torch.bfloat16, device=self.device)
+        B.cobalt_node_combine(self.eo, self.pos, self.assigned, self.gates, self.node_pos, w.N,
+                              w.g, self.node_partial, self.y_node, stream=stream)
+
     def ema(self, decay: float, flags: int = 0, stream=None):
         """Folds the accumulated counts into the planner EMAs (ema_coact,
         ema_count) and writes the Ochiai similarity of the counts; buffers are

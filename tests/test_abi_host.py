@@ -130,6 +130,16 @@ def test_argument_checks_reject_before_device_work():
     # combine: d not a multiple of 8, misaligned rows
     assert L.cobalt_combine(fake, fake, fake, 8, 2, 12, fake, None, None) == EINVAL
     assert L.cobalt_combine(_p(4098), fake, fake, 8, 2, 16, fake, None, None) == EINVAL
+    # node combine: null node_pos, d not a multiple of 8, N or g out of range,
+    # misaligned partial rows, T = 0 does nothing
+    cargs = [fake, fake, fake, fake]
+    assert L.cobalt_node_combine(*cargs, None, 8, 2, 2, 2, 16, fake, fake, None) == EINVAL
+    assert L.cobalt_node_combine(*cargs, fake, 8, 2, 2, 2, 12, fake, fake, None) == EINVAL
+    assert L.cobalt_node_combine(*cargs, fake, 8, 2, 17, 2, 16, fake, fake, None) == EINVAL
+    assert L.cobalt_node_combine(*cargs, fake, 8, 2, 2, 33, 16, fake, fake, None) == EINVAL
+    assert L.cobalt_node_combine(*cargs, fake, 8, 2, 2, 2, 16, _p(4104), fake, None) == EINVAL
+    assert L.cobalt_node_combine(None, None, None, None, None, 0, 2, 2, 2, 16, None, None,
+                                 None) == 0
 
 
 def test_layout_create_rejects_invalid_layouts_on_the_host(fig1):
