@@ -92,25 +92,20 @@ __global__ __launch_bounds__(kCombineWaves * 64) void combine_kernel(
 }
 
 // GROUPS = slices of 128 chunks per row, a template parameter so that the
-// block index splits into (token, slice) with a constant division; 0 takes
-// the count from groups_rt (rows wider than 16 slices). kUnit: every gate
-// is 1 and gates is not read (the source-side sum of the node-level
-// combine; fma(1, v, acc) rounds exactly as acc + v).
-template <bool kF32, int GROUPS, bool kUnit>
+// block index splits into (token, slice) with a constant division.
+template <bool kF32, int GROUPS>
 __global__ __launch_bounds__(kMaxK * 64) void fold_kernel(
     const u32x4* __restrict__ eo, const int32_t* __restrict__ pos, const float* __restrict__ gates,
-    int K, int64_t nch, int64_t TK, int groups_rt, u32x4* __restrict__ y,
-    float* __restrict__ y32) {
+    int K, int64_t nch, int64_t TK, u32x4* __restrict__ y, float* __restrict__ y32) {
     // K slices of 128 chunks (K * 2 KiB, sized at launch): a small stage
     // lets further workgroups start on a CU once the loading waves of a
     // workgroup have exited, which the wave count alone would not limit
     extern __shared__ u32x4 stage[];
     __shared__ float gate[kMaxK];
     __shared__ int valid[kMaxK];
-    const uint32_t groups = GROUPS ? GROUPS : (uint32_t)groups_rt;
     const uint32_t tg = blockIdx.x;
-    const uint32_t t = tg / groups;
-    const uint32_t g = tg - t * groups;
+    const uint32_t t = tg / GROUPS;
+    const uint32_t g = tg - t * GROUPS;
     const int j = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int64_t c0 = (int64_t)g * 128 + lane;
@@ -126,7 +121,7 @@ __global__ __launch_bounds__(kMaxK * 64) void fold_kernel(
         if (ok && in1) v1 = __builtin_nontemporal_load(row + c0 + 64);
         if (ok && in0) stage[j * 128 + lane] = v0;
         if (ok && in1) stage[j * 128 + lane + 64] = v1;
-        const float gj = kUnit ? 1.0f : gates[(int64_t)t * K + j];
+        const float gj = gates[(int64_t)t * K + j];
         if (lane == 0) {
             valid[j] = ok;
             gate[j] = gj;
@@ -160,22 +155,20 @@ __global__ __launch_bounds__(kMaxK * 64) void fold_kernel(
     if (kF32) *(float4*)(y32 + 2 * w) = make_float4(acc[0], acc[1], acc[2], acc[3]);
 }
 
-template <bool kF32, int GROUPS, bool kUnit>
+template <bool kF32, int GROUPS>
 bool try_fold(const void* eo, const int32_t* pos, const float* gates, int64_t T, int K,
-              int64_t nch, int64_t TK, void* y, float* y32, hipStream_t s) {
-    const int64_t groups = (nch + 127) / 128;
-    if constexpr (GROUPS > 0) {
-        if (groups != GROUPS)
-            return try_fold<kF32, GROUPS - 1, kUnit>(eo, pos, gates, T, K, nch, TK, y, y32, s);
-    } else if constexpr (!kUnit) {
-        return false;  // the plain combine has combine_kernel for wide rows
+              int64_t nch, void* y, float* y32, hipStream_t s) {
+    if constexpr (GROUPS == 0) {
+        return false;  // wider rows: combine_kernel
+    } else {
+        if ((nch + 127) / 128 != GROUPS)
+            return try_fold<kF32, GROUPS - 1>(eo, pos, gates, T, K, nch, y, y32, s);
+        if (T * GROUPS >= (int64_t(1) << 31)) return false;
+        hipLaunchKernelGGL((fold_kernel<kF32, GROUPS>), dim3((unsigned)(T * GROUPS)),
+                           dim3(std::max(K, kFoldWaves) * 64), (size_t)K * 128 * sizeof(u32x4), s,
+                           (const u32x4*)eo, pos, gates, K, nch, T * K, (u32x4*)y, y32);
+        return true;
     }
-    if (T * groups >= (int64_t(1) << 31)) return false;
-    hipLaunchKernelGGL((fold_kernel<kF32, GROUPS, kUnit>), dim3((unsigned)(T * groups)),
-                       dim3(std::max(K, kFoldWaves) * 64),
-                       (size_t)K * 128 * sizeof(u32x4), s,
-                       (const u32x4*)eo, pos, gates, K, nch, TK, (int)groups, (u32x4*)y, y32);
-    return true;
 }
 
 // Node side of the node-level combine: one workgroup per (token, 2 KiB
@@ -268,13 +261,106 @@ void launch_node_fold(const void* eo, const int32_t* pos, const int32_t* assigne
                        node_rows, (int)groups, (u32x4*)partial);
 }
 
+// Source side of the node-level combine: one workgroup of four waves per
+// (token, 2 KiB column slice). Wave j loads the node rows n = j, j + 4, ...
+// (SPW of them at most) that node_pos names for the token; after a barrier
+// the four waves sum the staged rows in increasing n, two 32-bit words per
+// thread, and store the slice of y. A token reaches only about half of the
+// nodes, so one wave per node would leave half the waves idle at the
+// barrier (1.91 ms against 1.65 ms on the T=131072, N=8, d=7168 workload).
+// GROUPS as for node_fold_kernel.
+template <int GROUPS, int SPW>
+__global__ __launch_bounds__(kFoldWaves * 64) void node_sum_kernel(
+    const u32x4* __restrict__ partial, const int32_t* __restrict__ node_pos, int N, int64_t nch,
+    int64_t node_rows, int groups_rt, u32x4* __restrict__ y) {
+    extern __shared__ u32x4 stage[];
+    __shared__ int valid[kMaxN];
+    const uint32_t groups = GROUPS ? GROUPS : (uint32_t)groups_rt;
+    const uint32_t tg = blockIdx.x;
+    const uint32_t t = tg / groups;
+    const uint32_t g = tg - t * groups;
+    const int j = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const int64_t c0 = (int64_t)g * 128 + lane;
+    // Lanes past the end of a ragged last slice load chunk 0 instead and
+    // stage values that no thread sums: with no lane-dependent branch around
+    // the loads, every row load is issued before the first wait (guarded
+    // loads here each waited for the one before).
+    const int64_t c0a = c0 < nch ? c0 : 0, c0b = c0 + 64 < nch ? c0 + 64 : 0;
+    u32x4 v[SPW][2];
+    bool ok[SPW];
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+        const int n = j + kFoldWaves * i;
+        const int q = n < N ? node_pos[(int64_t)t * N + n] : -1;
+        ok[i] = q >= 0 && q < node_rows;
+        if (ok[i]) {
+            const u32x4* row = partial + (int64_t)q * nch;
+            v[i][0] = __builtin_nontemporal_load(row + c0a);
+            v[i][1] = __builtin_nontemporal_load(row + c0b);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+        const int n = j + kFoldWaves * i;
+        if (n < N) {
+            if (ok[i]) {
+                stage[n * 128 + lane] = v[i][0];
+                stage[n * 128 + lane + 64] = v[i][1];
+            }
+            if (lane == 0) valid[n] = ok[i];
+        }
+    }
+    __syncthreads();
+    const int i = threadIdx.x;
+    const int64_t c = (int64_t)g * 128 + (i >> 1);
+    if (c >= nch) return;
+    const uint32_t* s32 = (const uint32_t*)stage;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int n = 0; n < N; ++n) {
+        if (!valid[n]) continue;
+        const u32x2 a = *(const u32x2*)(s32 + n * 512 + 2 * i);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            acc[2 * h] += __uint_as_float(a[h] << 16);
+            acc[2 * h + 1] += __uint_as_float(a[h] & 0xffff0000u);
+        }
+    }
+    u32x2 out;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+        out[h] = f32_to_bf16_rne(acc[2 * h]) | (f32_to_bf16_rne(acc[2 * h + 1]) << 16);
+    const int64_t w = ((int64_t)t * nch + (int64_t)g * 128) * 4 + 2 * i;
+    __builtin_nontemporal_store(out, (u32x2*)((uint32_t*)y + w));
+}
+
+template <int GROUPS>
+void launch_node_sum(const void* partial, const int32_t* node_pos, int64_t T, int N, int64_t nch,
+                     int64_t node_rows, void* y, hipStream_t s) {
+    const int64_t groups = (nch + 127) / 128;
+    if constexpr (GROUPS > 0) {
+        if (groups != GROUPS)
+            return launch_node_sum<GROUPS - 1>(partial, node_pos, T, N, nch, node_rows, y, s);
+    }
+    const dim3 grid((unsigned)(T * groups)), block(kFoldWaves * 64);
+    const size_t lds = (size_t)N * 128 * sizeof(u32x4);
+    if (N <= 2 * kFoldWaves)
+        hipLaunchKernelGGL((node_sum_kernel<GROUPS, 2>), grid, block, lds, s,
+                           (const u32x4*)partial, node_pos, N, nch, node_rows, (int)groups,
+                           (u32x4*)y);
+    else
+        hipLaunchKernelGGL((node_sum_kernel<GROUPS, 4>), grid, block, lds, s,
+                           (const u32x4*)partial, node_pos, N, nch, node_rows, (int)groups,
+                           (u32x4*)y);
+}
+
 }  // namespace
 
 cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* gates, int64_t T,
                              int K, int64_t d, void* y, float* y32, hipStream_t s) {
     const int64_t nch = d / 8;
-    if (y32 ? try_fold<true, 16, false>(eo, pos, gates, T, K, nch, T * K, y, y32, s)
-            : try_fold<false, 16, false>(eo, pos, gates, T, K, nch, T * K, y, y32, s)) {
+    if (y32 ? try_fold<true, 16>(eo, pos, gates, T, K, nch, y, y32, s)
+            : try_fold<false, 16>(eo, pos, gates, T, K, nch, y, y32, s)) {
         COBALT_LAUNCH_CHECK();
         return COBALT_OK;
     }
@@ -304,7 +390,7 @@ cobalt_status launch_node_combine(const void* eo, const int32_t* pos, const int3
                          partial, s);
     COBALT_LAUNCH_CHECK();
     // source side: y[t] = sum over n of partial[node_pos[t][n]], n increasing
-    try_fold<false, 16, true>(partial, node_pos, nullptr, T, N, nch, node_rows, y, nullptr, s);
+    launch_node_sum<16>(partial, node_pos, T, N, nch, node_rows, y, s);
     COBALT_LAUNCH_CHECK();
     return COBALT_OK;
 }
