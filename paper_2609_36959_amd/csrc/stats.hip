@@ -24,6 +24,13 @@
 //           depend on scheduling.
 // The workspace holds the partial histograms; its size comes from
 // cobalt_coact_stats_workspace_bytes.
+//
+// Small calls (one band, at most kDirectUpdates bin updates over all
+// chunks) skip the reduce: each count workgroup adds its nonzero bins
+// straight into coact and expert_count with integer atomics, whose sums do
+// not depend on their order. That saves the second launch, most of the time
+// of such a call; beyond the limit, contention on the atomics would cost
+// more than the reduce.
 #include <algorithm>
 #include <climits>
 #include <cmath>
@@ -42,6 +49,7 @@ constexpr int kReduceLanes = 8;  // lanes per bin in the reduce kernel
 constexpr int kMaxBands = 1024;
 constexpr int64_t kTokensPerChunk = 2048;
 constexpr int64_t kMaxChunks = 64;
+constexpr int64_t kDirectUpdates = 65536;
 
 struct Bands {
     int n;
@@ -121,6 +129,16 @@ bool make_plan(int64_t T, int E, int lds_bytes, Plan* p, Bands* bands) {
     return true;
 }
 
+// Row i of triangle bin w: the largest i with row_base(i) + i + 1 <= w.
+__device__ __forceinline__ int32_t tri_row(int32_t w, int32_t E) {
+    const int32_t words = E * (E - 1) / 2;
+    const int32_t r = words - 1 - w;  // index counted back from the last bin
+    int32_t q = (int32_t)((sqrtf(8.0f * (float)r + 1.0f) - 1.0f) * 0.5f);
+    while ((q + 1) * (q + 2) / 2 <= r) ++q;
+    while (q > 0 && q * (q + 1) / 2 > r) --q;
+    return E - 2 - q;
+}
+
 // KC = compile-time K (0: any K up to 16, read at run time). The ids of a
 // token are sorted first (invalid ids sort last as INT_MAX), so each pair
 // (a < b) has i = e[a] <= j = e[b] and costs one add on the row base of e[a].
@@ -128,7 +146,8 @@ template <bool kHalf, int KC>
 __global__ __launch_bounds__(kCountThreads) void coact_count_kernel(
     const int32_t* __restrict__ topk, int64_t T, int Kr, int E, Bands bands, int nchunks,
     int64_t tok_per_chunk, int64_t band_stride, uint32_t* __restrict__ part,
-    uint32_t* __restrict__ cpart) {
+    uint32_t* __restrict__ cpart, bool direct, uint32_t* __restrict__ coact,
+    uint32_t* __restrict__ count) {
     constexpr int KM = KC ? KC : kMaxK;
     const int K = KC ? KC : Kr;
     extern __shared__ uint32_t lds[];
@@ -196,6 +215,20 @@ __global__ __launch_bounds__(kCountThreads) void coact_count_kernel(
     }
     __syncthreads();
 
+    if (direct) {  // one band: the chunk's bins go straight to the outputs
+        for (int32_t bin = threadIdx.x; bin < nbins; bin += kCountThreads) {
+            const uint32_t v = kHalf ? (hist[bin >> 1] >> (16 * (bin & 1))) & 0xffffu : hist[bin];
+            if (v == 0) continue;
+            const int32_t i = tri_row(bin, E);
+            const int32_t j = bin - (row_base(i, E) + i + 1) + i + 1;
+            atomicAdd(&coact[(int64_t)i * E + j], v);
+            atomicAdd(&coact[(int64_t)j * E + i], v);
+        }
+        if (count)
+            for (int e = threadIdx.x; e < E; e += kCountThreads)
+                if (cnt[e]) atomicAdd(&count[e], cnt[e]);
+        return;
+    }
     uint32_t* out = part + (int64_t)blockIdx.x * band_stride;
     for (int32_t bin = threadIdx.x; bin < nbins; bin += kCountThreads)
         out[bin] = kHalf ? (hist[bin >> 1] >> (16 * (bin & 1))) & 0xffffu : hist[bin];
@@ -203,16 +236,6 @@ __global__ __launch_bounds__(kCountThreads) void coact_count_kernel(
         uint32_t* cout = cpart + (int64_t)chunk * E;
         for (int e = threadIdx.x; e < E; e += kCountThreads) cout[e] = cnt[e];
     }
-}
-
-// Row i of triangle bin w: the largest i with row_base(i) + i + 1 <= w.
-__device__ __forceinline__ int32_t tri_row(int32_t w, int32_t E) {
-    const int32_t words = E * (E - 1) / 2;
-    const int32_t r = words - 1 - w;  // index counted back from the last bin
-    int32_t q = (int32_t)((sqrtf(8.0f * (float)r + 1.0f) - 1.0f) * 0.5f);
-    while ((q + 1) * (q + 2) / 2 <= r) ++q;
-    while (q > 0 && q * (q + 1) / 2 > r) --q;
-    return E - 2 - q;
 }
 
 // kReduceLanes lanes per bin: lane k sums chunks k, k + kReduceLanes, ...;
@@ -272,9 +295,9 @@ cobalt_status launch_coact_stats(const int32_t* topk, int64_t T, int K, int E, u
     Bands bands;
     if (!make_plan(T, E, di.lds_bytes, &p, &bands)) return COBALT_EUNSUPPORTED;
     if (ws_bytes < p.part_bytes + p.count_bytes) return COBALT_EINVAL;
+    const bool direct = p.nbands == 1 && p.nchunks * (p.words + E) <= kDirectUpdates;
     uint32_t* part = (uint32_t*)ws;
     uint32_t* cpart = (uint32_t*)((char*)ws + p.part_bytes);
-    const dim3 grid((unsigned)(p.nchunks * p.nbands));
     // The LDS limit of each kernel variant is raised to the device maximum
     // once per device (host-side only, so the calls stay capturable).
     auto launch = [&](auto kernel, int variant) -> cobalt_status {
@@ -292,8 +315,9 @@ cobalt_status launch_coact_stats(const int32_t* topk, int64_t T, int K, int E, u
                 raised.insert({variant, dev});
             }
         }
-        hipLaunchKernelGGL(kernel, grid, dim3(kCountThreads), p.lds_bytes, s, topk, T, K, E,
-                           bands, p.nchunks, p.tok_per_chunk, p.band_stride, part, cpart);
+        hipLaunchKernelGGL(kernel, dim3((unsigned)(p.nchunks * p.nbands)), dim3(kCountThreads),
+                           p.lds_bytes, s, topk, T, K, E, bands, p.nchunks, p.tok_per_chunk,
+                           p.band_stride, part, cpart, direct, coact, count);
         return COBALT_OK;
     };
     cobalt_status st;
@@ -303,6 +327,7 @@ cobalt_status launch_coact_stats(const int32_t* topk, int64_t T, int K, int E, u
         st = p.half ? launch(coact_count_kernel<true, 0>, 2) : launch(coact_count_kernel<false, 0>, 3);
     if (st != COBALT_OK) return st;
     COBALT_LAUNCH_CHECK();
+    if (direct) return COBALT_OK;
     const int64_t items = (p.words + (count ? E : 0)) * kReduceLanes;
     hipLaunchKernelGGL(coact_reduce_kernel,
                        dim3((unsigned)((items + kReduceThreads - 1) / kReduceThreads)),
