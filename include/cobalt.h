@@ -96,8 +96,10 @@ cobalt_status cobalt_layout_tables(cobalt_layout_t layout, uint32_t* host_node_m
  *   T, K, E) bytes (partial histograms, about 4 * min(64, T/2048) * E(E-1)/2
  *   bytes), 256-byte aligned, owned by the caller; contents on entry are
  *   ignored; it must not be shared by calls that may overlap. The call
- *   updates coact and expert_count with plain (non-atomic) adds, so calls
- *   that may overlap must not share them either.
+ *   updates coact and expert_count with plain (non-atomic) adds, or with
+ *   integer atomic adds when it is small (at most 65536 bin updates), so
+ *   calls that may overlap must not share them either. The counts are exact
+ *   either way and do not depend on scheduling.
  * ---------------------------------------------------------------------- */
 size_t cobalt_coact_stats_workspace_bytes(int64_t T, int32_t K, int32_t E);
 
