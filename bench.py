@@ -300,8 +300,8 @@ def cpu_baseline(st, n_tokens, torch, W, PL):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path has "
-              "no inter-GPU collectives in this build", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has "
+              "no inter-GPU collectives; its virtual ranks are buffers on one GPU", file=sys.stderr)
         sys.exit(2)
     import torch
 

@@ -37,13 +37,13 @@ extern "C" {
 typedef enum {
     COBALT_OK = 0,
     COBALT_EINVAL = 1,       /* bad argument (null pointer, size out of range, misaligned) */
-    COBALT_EUNSUPPORTED = 2, /* valid request outside this build's limits */
+    COBALT_EUNSUPPORTED = 2, /* valid request outside the library's limits */
     COBALT_ENOMEM = 3,       /* device allocation failed (layout calls only) */
     COBALT_EHIP = 4,         /* a HIP runtime call or kernel launch failed */
     COBALT_EDATA = 5         /* input data violates the model (layout or routing) */
 } cobalt_status;
 
-/* Limits of this build: 1 <= N <= 16, 1 <= gpus_per_node <= 32,
+/* Limits of the library: 1 <= N <= 16, 1 <= gpus_per_node <= 32,
  * G = N * gpus_per_node <= 512, 1 <= K <= 16, 1 <= E <= 4096,
  * T * K < 2^31, d % 8 == 0 (rows are whole 16-byte vectors). */
 
