@@ -311,7 +311,8 @@ cobalt_status cobalt_intra_node_rebalance(int32_t N, int32_t gpus_per_node, int3
  * to 1/256 so that every comparison of gains is exact.
  *
  * host_coact_ema [E][E] fp32 in: c_ij (EMA of co-activation counts; only
- *   i < j is read; finite, >= 0, <= 2^40).
+ *   i < j is read; finite, >= 0, <= 2^28, so that every integer sum of the
+ *   quantised weights fits in int64).
  * host_count_ema [E] fp32 in: w_e (EMA of expert task counts; finite, >= 0).
  * eps: the allowed imbalance (>= 0; the paper's default is 0.15).
  * host_slot_table [G][S] int32 out: expert ids, -1 for empty slots.

@@ -842,7 +842,7 @@ int ref_plan_layout(int32_t N, int32_t g, int32_t E, int32_t S, const float* coa
                     const float* count_ema, float eps, int32_t* slot_table, int32_t* owner,
                     float* plan, double* objective, int32_t* feasible)
 {
-    if (N < 1 || N > 16 || g < 1 || g > 32 || E < 1 || S < 1) return REF_EINVAL;
+    if (N < 1 || N > 16 || g < 1 || g > 32 || E < 1 || E > 4096 || S < 1) return REF_EINVAL;
     if (!(eps >= 0.0f) || isinf(eps)) return REF_EINVAL;
     int32_t G = N * g;
     if ((int64_t)G * S < E) return REF_EINVAL;
@@ -851,7 +851,9 @@ int ref_plan_layout(int32_t N, int32_t g, int32_t E, int32_t S, const float* coa
     for (int32_t i = 0; i < E; ++i)
         for (int32_t j = i + 1; j < E; ++j) {
             float c = coact_ema[(int64_t)i * E + j];
-            if (!(c >= 0.0f) || !(c <= 1099511627776.0f)) return REF_EDATA; /* 2^40 */
+            /* q <= 2^36: the objective, at most 16 nodes x E(E-1)/2 < 2^23 */
+            /* pairs of them, stays below 2^63 */
+            if (!(c >= 0.0f) || !(c <= 268435456.0f)) return REF_EDATA; /* 2^28 */
         }
 
     int rc = REF_OK;

@@ -467,7 +467,9 @@ extern "C" cobalt_status cobalt_plan_layout(int32_t N, int32_t gpn, int32_t E, i
     for (int i = 0; i < E; ++i)
         for (int j = i + 1; j < E; ++j) {
             const float c = coact_ema[(size_t)i * E + j];
-            if (!(c >= 0.0f) || !(c <= 1099511627776.0f)) return COBALT_EDATA;  // 2^40
+            // q <= 2^36: the objective, at most kMaxN nodes x E(E-1)/2 < 2^23
+            // pairs of them, stays below 2^63
+            if (!(c >= 0.0f) || !(c <= 268435456.0f)) return COBALT_EDATA;  // 2^28
         }
 
     Planner P;

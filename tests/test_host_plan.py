@@ -71,11 +71,18 @@ def test_library_rejects_what_the_oracle_rejects():
     one = np.ones(8, np.float32)
     bad = z.copy()
     bad[0, 1] = np.nan
+    huge = z.copy()
+    huge[0, 1] = 2.0**29
     for args in ((2, 2, 8, 1, z, one, 0.1),             # G*S < E
                  (2, 2, 8, 2, bad, one, 0.1),           # NaN pair weight
+                 (2, 2, 8, 2, huge, one, 0.1),          # pair weight above 2^28
                  (2, 2, 8, 2, z, -one, 0.1),            # negative workload
                  (2, 2, 8, 2, z, one, -1.0)):           # negative eps
         with pytest.raises(B.CobaltError):
             B.cobalt_plan_layout(*args)
         with pytest.raises(oracle.OracleError):
             oracle.plan_layout(*args)
+    # the largest pair weight accepted: both plan it, identically
+    edge = z.copy()
+    edge[0, 1] = edge[1, 0] = 2.0**28
+    same(2, 2, 8, 2, edge, one, 0.1)
