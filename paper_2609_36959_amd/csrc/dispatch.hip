@@ -30,8 +30,8 @@
 // where prefix_n(t) counts the tokens before t that reach node n: an N-way
 // prefix count over tokens, done with ballots per node bit and the same
 // decoupled look-back. The same init and scan kernels serve both; the node
-// rows are written by copy_kernel, one wave storing its slice of x[t] to all
-// of the token's node rows.
+// rows are written by node_scatter_kernel, four waves per (token, slice)
+// with two or four nodes each (copy_kernel for rows wider than 16 slices).
 #include <algorithm>
 
 #include "internal.hpp"
@@ -568,6 +568,69 @@ bool try_scatter<0>(const void*, const int32_t*, int64_t, int, int64_t, int64_t,
     return false;
 }
 
+// Row scatter for the node-deduplicated layout: one workgroup of
+// kNodeScatterWaves waves per (token, 2 KiB column slice); wave j loads the
+// slice of x[t] and stores it to the token's rows for nodes n = j, j + 4,
+// ... (SPW of them at most). A token has rows on only about half of the
+// nodes, so one wave per node would leave half of the waves without a row
+// (2.06 ms) and one wave for all of the token's rows serialises their
+// stores (1.99 ms); two nodes per wave take 1.63 ms on the T=131072, N=8,
+// d=7168 workload. GROUPS as for scatter_kernel.
+constexpr int kNodeScatterWaves = 4;
+
+template <int GROUPS, int SPW>
+__global__ __launch_bounds__(kNodeScatterWaves * 64) void node_scatter_kernel(
+    const u32x4* __restrict__ x, const int32_t* __restrict__ node_pos, int N, int64_t nch,
+    int64_t bound, u32x4* __restrict__ packed) {
+    const uint32_t tg = blockIdx.x;
+    const uint32_t t = tg / GROUPS;
+    const uint32_t g = tg - t * GROUPS;
+    const int j = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t c0 = (int64_t)g * 128 + (threadIdx.x & 63);
+    // loads first, as in scatter_kernel (the guards keep them there)
+    const u32x4* row = x + (int64_t)t * nch;
+    const bool in0 = c0 < nch, in1 = c0 + 64 < nch;
+    u32x4 v0, v1;
+    if (in0) v0 = row[c0];
+    if (in1) v1 = row[c0 + 64];
+    int q[SPW];
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+        const int n = j + kNodeScatterWaves * i;
+        q[i] = n < N ? node_pos[(int64_t)t * N + n] : -1;
+    }
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+        if (q[i] < 0 || q[i] >= bound) continue;
+        u32x4* dst = packed + (int64_t)q[i] * nch;
+        if (in0) __builtin_nontemporal_store(v0, dst + c0);
+        if (in1) __builtin_nontemporal_store(v1, dst + c0 + 64);
+    }
+}
+
+// Launches node_scatter_kernel when the slice count has an instantiation and
+// the block count fits; returns false otherwise (the caller then uses the
+// fan-out copy).
+template <int GROUPS>
+bool try_node_scatter(const void* x, const int32_t* node_pos, int64_t T, int N, int64_t nch,
+                      int64_t bound, void* packed, hipStream_t s) {
+    if constexpr (GROUPS == 0) {
+        return false;
+    } else {
+        if ((nch + 127) / 128 != GROUPS)
+            return try_node_scatter<GROUPS - 1>(x, node_pos, T, N, nch, bound, packed, s);
+        if (T * GROUPS >= (int64_t(1) << 31)) return false;
+        const dim3 grid((unsigned)(T * GROUPS)), block(kNodeScatterWaves * 64);
+        if (N <= 2 * kNodeScatterWaves)
+            hipLaunchKernelGGL((node_scatter_kernel<GROUPS, 2>), grid, block, 0, s,
+                               (const u32x4*)x, node_pos, N, nch, bound, (u32x4*)packed);
+        else
+            hipLaunchKernelGGL((node_scatter_kernel<GROUPS, 4>), grid, block, 0, s,
+                               (const u32x4*)x, node_pos, N, nch, bound, (u32x4*)packed);
+        return true;
+    }
+}
+
 // Copies x[t] to the rows pos[t][0..per_tok) that are in [0, bound).
 template <bool kNode>
 cobalt_status launch_copy(const void* x, const int32_t* pos, int64_t T, int per_tok, int64_t d,
@@ -694,11 +757,12 @@ cobalt_status launch_node_dispatch(const int32_t* assigned, const int32_t* src, 
                            w.status, node_pos, fwd, row_token);
     COBALT_LAUNCH_CHECK();
     if (!x) return COBALT_OK;
-    // The fan-out copy, not scatter_kernel: a token has rows on about half
-    // of the nodes, so one wave per (token, slice, node) would leave half
-    // the waves without a row (2.14 ms against 2.01 ms on the T=131072,
-    // E=256 workload).
-    return launch_copy<true>(x, node_pos, T, N, d, T * std::min(K, N), packed, s);
+    const int64_t bound = T * std::min(K, N);
+    if (try_node_scatter<16>(x, node_pos, T, N, d / 8, bound, packed, s)) {
+        COBALT_LAUNCH_CHECK();
+        return COBALT_OK;
+    }
+    return launch_copy<true>(x, node_pos, T, N, d, bound, packed, s);
 }
 
 }  // namespace cobalt
