@@ -9,12 +9,16 @@
 // K slices in slot order, two 32-bit words per thread, and store the slice
 // of y. Each wave has a single row to fetch, so many independent row loads
 // are in flight; on the T=131072, K=8, d=7168 workload this runs at
-// 6.1-6.2 TB/s, against 5.6 TB/s for combine_kernel. Folding with one wave
+// 6.3-6.4 TB/s, against 5.6 TB/s for combine_kernel. Folding with one wave
 // (two chunks per lane) instead holds the stage longer and costs 2 %.
 //
 // combine_kernel (other shapes): each wave takes one (token, 1 KiB slice)
 // and loads the chunks of all K rows itself, issuing every load before its
 // single store so that no load waits behind a store.
+//
+// The node-level combine (the reverse of the node-deduplicated dispatch)
+// follows: node_fold_kernel sums each node's slots into a bf16 partial row,
+// node_sum_kernel sums a token's partial rows in node order.
 #include <algorithm>
 
 #include "internal.hpp"
