@@ -557,6 +557,24 @@ def main():
         "hbm_frac": cb / (ncb_ms * 1e-3) / HBM_PEAK, "node_combine_ms": ncb_ms,
         "pair_combine_ms": call_ms["cobalt_combine"],
         "cross_node_rows": rows - local_rows}
+    # the step as a node-deduplicating transport would run it: statistics,
+    # assignment, node-deduplicated pack and node-level combine
+    def node_step():
+        st.stats(stream=stream)
+        st.assign(stream=stream)
+        st.node_pack(stream=stream)
+        st.node_combine(stream=stream)
+    with torch.cuda.stream(stream):
+        node_step()
+        ev[0].record(stream)
+        for _ in range(args.steps):
+            node_step()
+        ev[1].record(stream)
+    torch.cuda.synchronize()
+    nstep_ms = ev[0].elapsed_time(ev[1]) / args.steps
+    result["node_dedup_step"] = {"ms_per_step": nstep_ms, "value": w.T / (nstep_ms * 1e-3),
+                                 "unit": "tokens/s",
+                                 "calls": "stats + assign + node_dispatch_pack + node_combine"}
     # planner statistics of one step: EMA update of the co-activation and
     # expert counts, and the Ochiai similarity (the Fig. 3 statistic)
     st.coact.zero_()
