@@ -1,6 +1,7 @@
 // C entry points: argument checks, the layout handle, and dispatch to the
 // kernel launchers.
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <vector>
@@ -160,6 +161,18 @@ extern "C" cobalt_status cobalt_layout_tables(cobalt_layout_t L, uint32_t* node_
 }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+namespace cobalt {
+int64_t max_launch_items() {
+    const char* v = std::getenv("COBALT_MAX_LAUNCH_ITEMS");
+    if (!v || !*v) return kMaxLaunchItems;
+    char* end = nullptr;
+    const long long n = std::strtoll(v, &end, 10);
+    if (*end != '\0' || n < 64) return kMaxLaunchItems;
+    return n < kMaxLaunchItems ? (int64_t)n : kMaxLaunchItems;
+}
+}  // namespace cobalt
+
 
 extern "C" size_t cobalt_coact_stats_workspace_bytes(int64_t T, int32_t K, int32_t E) {
     if (T < 0 || K < 1 || K > kMaxK || E < 1 || E > kMaxE) return 0;

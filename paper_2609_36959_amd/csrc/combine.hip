@@ -167,10 +167,13 @@ bool try_fold(const void* eo, const int32_t* pos, const float* gates, int64_t T,
     } else {
         if ((nch + 127) / 128 != GROUPS)
             return try_fold<kF32, GROUPS - 1>(eo, pos, gates, T, K, nch, y, y32, s);
-        if (T * GROUPS >= (int64_t(1) << 31)) return false;
-        hipLaunchKernelGGL((fold_kernel<kF32, GROUPS>), dim3((unsigned)(T * GROUPS)),
-                           dim3(std::max(K, kFoldWaves) * 64), (size_t)K * 128 * sizeof(u32x4), s,
-                           (const u32x4*)eo, pos, gates, K, nch, T * K, (u32x4*)y, y32);
+        const int threads = std::max(K, kFoldWaves) * 64;
+        for_token_ranges(T, (int64_t)GROUPS * threads, [&](int64_t t0, int64_t n) {
+            hipLaunchKernelGGL((fold_kernel<kF32, GROUPS>), dim3((unsigned)(n * GROUPS)),
+                               dim3(threads), (size_t)K * 128 * sizeof(u32x4), s,
+                               (const u32x4*)eo, pos + t0 * K, gates + t0 * K, K, nch, T * K,
+                               (u32x4*)y + t0 * nch, y32 ? y32 + t0 * nch * 8 : nullptr);
+        });
         return true;
     }
 }
@@ -270,10 +273,13 @@ void launch_node_fold(const void* eo, const int32_t* pos, const int32_t* assigne
             return launch_node_fold<GROUPS - 1>(eo, pos, assigned, gates, node_pos, T, K, N, gpn,
                                                 nch, node_rows, partial, s);
     }
-    hipLaunchKernelGGL(node_fold_kernel<GROUPS>, dim3((unsigned)(T * groups)),
-                       dim3(std::max(K, kFoldWaves) * 64), (size_t)K * 128 * sizeof(u32x4), s,
-                       (const u32x4*)eo, pos, assigned, gates, node_pos, K, N, gpn, nch, T * K,
-                       node_rows, (int)groups, (u32x4*)partial);
+    const int threads = std::max(K, kFoldWaves) * 64;
+    for_token_ranges(T, groups * threads, [&](int64_t t0, int64_t n) {
+        hipLaunchKernelGGL(node_fold_kernel<GROUPS>, dim3((unsigned)(n * groups)), dim3(threads),
+                           (size_t)K * 128 * sizeof(u32x4), s, (const u32x4*)eo, pos + t0 * K,
+                           assigned + t0 * K, gates + t0 * K, node_pos + t0 * N, K, N, gpn, nch,
+                           T * K, node_rows, (int)groups, (u32x4*)partial);
+    });
 }
 
 // Source side of the node-level combine: one workgroup of four waves per
@@ -357,16 +363,19 @@ void launch_node_sum(const void* partial, const int32_t* node_pos, int64_t T, in
         if (groups != GROUPS)
             return launch_node_sum<GROUPS - 1>(partial, node_pos, T, N, nch, node_rows, y, s);
     }
-    const dim3 grid((unsigned)(T * groups)), block(kFoldWaves * 64);
+    const dim3 block(kFoldWaves * 64);
     const size_t lds = (size_t)N * 128 * sizeof(u32x4);
-    if (N <= 2 * kFoldWaves)
-        hipLaunchKernelGGL((node_sum_kernel<GROUPS, 2>), grid, block, lds, s,
-                           (const u32x4*)partial, node_pos, N, nch, node_rows, (int)groups,
-                           (u32x4*)y);
-    else
-        hipLaunchKernelGGL((node_sum_kernel<GROUPS, 4>), grid, block, lds, s,
-                           (const u32x4*)partial, node_pos, N, nch, node_rows, (int)groups,
-                           (u32x4*)y);
+    for_token_ranges(T, groups * kFoldWaves * 64, [&](int64_t t0, int64_t n) {
+        const dim3 grid((unsigned)(n * groups));
+        if (N <= 2 * kFoldWaves)
+            hipLaunchKernelGGL((node_sum_kernel<GROUPS, 2>), grid, block, lds, s,
+                               (const u32x4*)partial, node_pos + t0 * N, N, nch, node_rows,
+                               (int)groups, (u32x4*)y + t0 * nch);
+        else
+            hipLaunchKernelGGL((node_sum_kernel<GROUPS, 4>), grid, block, lds, s,
+                               (const u32x4*)partial, node_pos + t0 * N, N, nch, node_rows,
+                               (int)groups, (u32x4*)y + t0 * nch);
+    });
 }
 
 }  // namespace
@@ -379,11 +388,15 @@ cobalt_status launch_combine(const void* eo, const int32_t* pos, const float* ga
         COBALT_LAUNCH_CHECK();
         return COBALT_OK;
     }
-    const int64_t items = T * ((nch + 63) / 64);
-    const dim3 grid((unsigned)((items + kCombineWaves - 1) / kCombineWaves));
+    const int64_t g64 = (nch + 63) / 64;  // one wave per (token, 1 KiB slice)
     auto launch = [&](auto kernel) {
-        hipLaunchKernelGGL(kernel, grid, dim3(kCombineWaves * 64), 0, s, (const u32x4*)eo, pos,
-                           gates, T, K, nch, T * K, (u32x4*)y, y32);
+        for_token_ranges(T, g64 * 64, [&](int64_t t0, int64_t n) {
+            const int64_t items = n * g64;
+            hipLaunchKernelGGL(kernel, dim3((unsigned)((items + kCombineWaves - 1) / kCombineWaves)),
+                               dim3(kCombineWaves * 64), 0, s, (const u32x4*)eo, pos + t0 * K,
+                               gates + t0 * K, n, K, nch, T * K, (u32x4*)y + t0 * nch,
+                               y32 ? y32 + t0 * nch * 8 : nullptr);
+        });
     };
     if (K == 8)
         y32 ? launch(combine_kernel<true, 8>) : launch(combine_kernel<false, 8>);
@@ -398,8 +411,6 @@ cobalt_status launch_node_combine(const void* eo, const int32_t* pos, const int3
                                   int N, int gpn, int64_t d, void* partial, void* y,
                                   hipStream_t s) {
     const int64_t nch = d / 8;
-    const int64_t groups = (nch + 127) / 128;
-    if (T * groups >= (int64_t(1) << 31)) return COBALT_EUNSUPPORTED;
     const int64_t node_rows = T * std::min(K, N);
     launch_node_fold<16>(eo, pos, assigned, gates, node_pos, T, K, N, gpn, nch, node_rows,
                          partial, s);

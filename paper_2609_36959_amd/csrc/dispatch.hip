@@ -550,16 +550,18 @@ __global__ __launch_bounds__(kMaxK * 64) void scatter_kernel(
 }
 
 // Launches scatter_kernel for rows pos[t][0..per_tok) in [0, bound) when
-// the slice count has an instantiation and the block count fits; returns
-// false otherwise (the caller then uses the fan-out copy).
+// the slice count has an instantiation; returns false otherwise (the
+// caller then uses the fan-out copy).
 template <int GROUPS>
 bool try_scatter(const void* x, const int32_t* pos, int64_t T, int per_tok, int64_t nch,
                  int64_t bound, void* packed, hipStream_t s) {
     if ((nch + 127) / 128 != GROUPS)
         return try_scatter<GROUPS - 1>(x, pos, T, per_tok, nch, bound, packed, s);
-    if (T * GROUPS >= (int64_t(1) << 31)) return false;
-    hipLaunchKernelGGL(scatter_kernel<GROUPS>, dim3((unsigned)(T * GROUPS)), dim3(per_tok * 64),
-                       0, s, (const u32x4*)x, pos, per_tok, nch, bound, (u32x4*)packed);
+    for_token_ranges(T, (int64_t)GROUPS * per_tok * 64, [&](int64_t t0, int64_t n) {
+        hipLaunchKernelGGL(scatter_kernel<GROUPS>, dim3((unsigned)(n * GROUPS)),
+                           dim3(per_tok * 64), 0, s, (const u32x4*)x + t0 * nch,
+                           pos + t0 * per_tok, per_tok, nch, bound, (u32x4*)packed);
+    });
     return true;
 }
 template <>
@@ -608,9 +610,8 @@ __global__ __launch_bounds__(kNodeScatterWaves * 64) void node_scatter_kernel(
     }
 }
 
-// Launches node_scatter_kernel when the slice count has an instantiation and
-// the block count fits; returns false otherwise (the caller then uses the
-// fan-out copy).
+// Launches node_scatter_kernel when the slice count has an instantiation;
+// returns false otherwise (the caller then uses the fan-out copy).
 template <int GROUPS>
 bool try_node_scatter(const void* x, const int32_t* node_pos, int64_t T, int N, int64_t nch,
                       int64_t bound, void* packed, hipStream_t s) {
@@ -619,14 +620,18 @@ bool try_node_scatter(const void* x, const int32_t* node_pos, int64_t T, int N, 
     } else {
         if ((nch + 127) / 128 != GROUPS)
             return try_node_scatter<GROUPS - 1>(x, node_pos, T, N, nch, bound, packed, s);
-        if (T * GROUPS >= (int64_t(1) << 31)) return false;
-        const dim3 grid((unsigned)(T * GROUPS)), block(kNodeScatterWaves * 64);
-        if (N <= 2 * kNodeScatterWaves)
-            hipLaunchKernelGGL((node_scatter_kernel<GROUPS, 2>), grid, block, 0, s,
-                               (const u32x4*)x, node_pos, N, nch, bound, (u32x4*)packed);
-        else
-            hipLaunchKernelGGL((node_scatter_kernel<GROUPS, 4>), grid, block, 0, s,
-                               (const u32x4*)x, node_pos, N, nch, bound, (u32x4*)packed);
+        const dim3 block(kNodeScatterWaves * 64);
+        for_token_ranges(T, (int64_t)GROUPS * kNodeScatterWaves * 64, [&](int64_t t0, int64_t n) {
+            const dim3 grid((unsigned)(n * GROUPS));
+            const u32x4* xr = (const u32x4*)x + t0 * nch;
+            const int32_t* np = node_pos + t0 * N;
+            if (N <= 2 * kNodeScatterWaves)
+                hipLaunchKernelGGL((node_scatter_kernel<GROUPS, 2>), grid, block, 0, s, xr, np, N,
+                                   nch, bound, (u32x4*)packed);
+            else
+                hipLaunchKernelGGL((node_scatter_kernel<GROUPS, 4>), grid, block, 0, s, xr, np, N,
+                                   nch, bound, (u32x4*)packed);
+        });
         return true;
     }
 }
@@ -639,9 +644,13 @@ cobalt_status launch_copy(const void* x, const int32_t* pos, int64_t T, int per_
     const u32x4* xv = (const u32x4*)x;
     u32x4* pv = (u32x4*)packed;
     auto launch = [&](auto kernel, int64_t cg) {
-        const int64_t items = T * ((nch + 64 * cg - 1) / (64 * cg));
-        hipLaunchKernelGGL(kernel, dim3((unsigned)((items + kCopyWaves - 1) / kCopyWaves)),
-                           dim3(kCopyWaves * 64), 0, s, xv, pos, T, per_tok, nch, bound, pv);
+        const int64_t groups = (nch + 64 * cg - 1) / (64 * cg);  // one wave each
+        for_token_ranges(T, groups * 64, [&](int64_t t0, int64_t n) {
+            const int64_t items = n * groups;
+            hipLaunchKernelGGL(kernel, dim3((unsigned)((items + kCopyWaves - 1) / kCopyWaves)),
+                               dim3(kCopyWaves * 64), 0, s, xv + t0 * nch, pos + t0 * per_tok, n,
+                               per_tok, nch, bound, pv);
+        });
     };
     if (nch >= 128)
         per_tok == 8 ? launch(copy_kernel<2, 8, kNode>, 2) : launch(copy_kernel<2, 0, kNode>, 2);

@@ -30,6 +30,30 @@ struct DeviceLayout {
     int32_t* owner;            // [E]
 };
 
+// A dispatch packet holds the grid size in work-items as a 32-bit value,
+// and a larger grid is cut short without an error. Kernels that take one
+// workgroup (or wave) per token slice are therefore launched over ranges of
+// tokens of at most max_launch_items() work-items each, with their
+// per-token arrays offset to the range; the rows they address through pos
+// or node_pos stay absolute.
+constexpr int64_t kMaxLaunchItems = int64_t(1) << 31;
+
+// kMaxLaunchItems, or a smaller limit from the environment variable
+// COBALT_MAX_LAUNCH_ITEMS (read at every launch, at least 64), so that
+// tests can split ordinary sizes into many ranges.
+int64_t max_launch_items();
+
+// Calls launch(t0, n) for consecutive token ranges [t0, t0 + n) covering
+// [0, T), each of at most max_launch_items() / items_per_token tokens (at
+// least one).
+template <typename F>
+void for_token_ranges(int64_t T, int64_t items_per_token, F&& launch) {
+    const int64_t per = items_per_token > 0 ? items_per_token : 1;
+    const int64_t lim = max_launch_items();
+    const int64_t step = lim / per > 0 ? lim / per : 1;
+    for (int64_t t0 = 0; t0 < T; t0 += step) launch(t0, T - t0 < step ? T - t0 : step);
+}
+
 #define COBALT_LAUNCH_CHECK()                                        \
     do {                                                             \
         if (hipGetLastError() != hipSuccess) return COBALT_EHIP;     \
