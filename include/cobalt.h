@@ -201,6 +201,21 @@ cobalt_status cobalt_node_dispatch_pack(const int32_t* assigned_rank, const int3
                                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Step 4: combine and weighted sum (Fig. 1, last stage).
+ *
+ * expert_out [T*K][d] bf16 in, in the packed layout (row pos[p] holds the
+ * result of pair p); pos [T][K] int32 in; gates [T][K] fp32 in.
+ * y [T][d] bf16 out:
+ *   y[t][c] = bf16_rne( sum_{j=0..K-1} gates[t][j] * expert_out[pos[t][j]][c] )
+ * accumulated in fp32 from 0 with one fused multiply-add per slot in slot
+ * order. y_f32 [T][d] fp32 out (may be NULL) receives the fp32 sums. A pos
+ * outside [0, T*K) contributes nothing.
+ * ---------------------------------------------------------------------- */
+cobalt_status cobalt_combine(const void* expert_out, const int32_t* pos, const float* gates,
+                             int64_t T, int32_t K, int64_t d,
+                             void* y, float* y_f32, void* stream);
+
+/* ------------------------------------------------------------------------
  * Step 4': node-level combine, the reverse of the node-deduplicated
  * dispatch (Section 1 and Section 3.1: a token's results leave a node once,
  * so the combine's cross-node rows also number Eq. 1's V).
@@ -232,21 +247,6 @@ cobalt_status cobalt_node_combine(const void* expert_out, const int32_t* pos,
                                   const int32_t* node_pos, int64_t T, int32_t K, int32_t N,
                                   int32_t gpus_per_node, int64_t d, void* node_partial, void* y,
                                   void* stream);
-
-/* ------------------------------------------------------------------------
- * Step 4: combine and weighted sum (Fig. 1, last stage).
- *
- * expert_out [T*K][d] bf16 in, in the packed layout (row pos[p] holds the
- * result of pair p); pos [T][K] int32 in; gates [T][K] fp32 in.
- * y [T][d] bf16 out:
- *   y[t][c] = bf16_rne( sum_{j=0..K-1} gates[t][j] * expert_out[pos[t][j]][c] )
- * accumulated in fp32 from 0 with one fused multiply-add per slot in slot
- * order. y_f32 [T][d] fp32 out (may be NULL) receives the fp32 sums. A pos
- * outside [0, T*K) contributes nothing.
- * ---------------------------------------------------------------------- */
-cobalt_status cobalt_combine(const void* expert_out, const int32_t* pos, const float* gates,
-                             int64_t T, int32_t K, int64_t d,
-                             void* y, float* y_f32, void* stream);
 
 /* ------------------------------------------------------------------------
  * Per-replica workload (Section 3.1 workload model: w_er counts the tasks of
