@@ -777,6 +777,12 @@ done:
 /*    w_x, cap - load_u + w_x, l_eh,h) of eh moves to a new replica on u, */
 /*    if m > w_x. Stop when neither applies or a path move is below       */
 /*    cap 1e-12 (at most 4 g^2 S moves).                                  */
+/* 2b. Global repair. The same augmenting-path search over the ranks of  */
+/*    all nodes (ranks in increasing id), so that a node left above its   */
+/*    ranks' caps can pass work to replicas, or new replicas in free      */
+/*    slots, on other nodes: a new replica makes its expert a member of   */
+/*    that node. It stops when no rank exceeds cap, no rank below cap is  */
+/*    reachable, or a move is below cap 1e-12 (at most 4 G S moves).      */
 /* 3. Co-activation replicas. While some (e, n) with e not on n, a free   */
 /*    slot on n and positive gain exists: add the one with the largest    */
 /*    gain (ties: larger w, smaller e, smaller n) on the rank of n with   */
@@ -1241,6 +1247,71 @@ int ref_plan_layout(int32_t N, int32_t g, int32_t E, int32_t S, const float* coa
         }
         used[n] = 0;
         for (int32_t i = 0; i < g; ++i) used[n] += plan_used(slot_table, S, n * g + i);
+    }
+
+    /* 2b. global repair: augmenting paths over the ranks of all nodes */
+    {
+        int32_t* gq = (int32_t*)malloc((size_t)G * sizeof(int32_t));
+        int32_t* gp = (int32_t*)malloc((size_t)G * sizeof(int32_t));
+        int32_t* gv = (int32_t*)malloc((size_t)G * sizeof(int32_t));
+        uint8_t* gs = (uint8_t*)malloc((size_t)G);
+        if (!gq || !gp || !gv || !gs) {
+            free(gq); free(gp); free(gv); free(gs);
+            rc = REF_EINVAL;
+            goto done;
+        }
+        for (int64_t moves = 0; moves < 4 * (int64_t)G * S; ++moves) {
+            int32_t h = -1;
+            double hl = 0.0;
+            for (int32_t r = 0; r < G; ++r) {
+                double l = plan_rank_load(pl, E, G, r);
+                if (h < 0 || l > hl) {
+                    h = r;
+                    hl = l;
+                }
+            }
+            if (!(hl > cap)) break;
+            int32_t qh = 0, qt = 0, target = -1;
+            for (int32_t r = 0; r < G; ++r) gs[r] = 0;
+            gq[qt++] = h;
+            gs[h] = 1;
+            while (qh < qt && target < 0) {
+                int32_t a = gq[qh++];
+                for (int32_t e = 0; e < E && target < 0; ++e) {
+                    if (!(pl[(int64_t)e * G + a] > 0.0)) continue;
+                    for (int32_t b = 0; b < G && target < 0; ++b) {
+                        if (gs[b]) continue;
+                        if (!plan_holds(slot_table, S, b, e) && plan_used(slot_table, S, b) >= S)
+                            continue;
+                        gs[b] = 1;
+                        gp[b] = a;
+                        gv[b] = e;
+                        gq[qt++] = b;
+                        if (plan_rank_load(pl, E, G, b) < cap) target = b;
+                    }
+                }
+            }
+            if (target < 0) break;
+            double mv = hl - cap;
+            double room = cap - plan_rank_load(pl, E, G, target);
+            if (room < mv) mv = room;
+            for (int32_t b = target; b != h; b = gp[b]) {
+                double avail = pl[(int64_t)gv[b] * G + gp[b]];
+                if (avail < mv) mv = avail;
+            }
+            if (!(mv > cap * 1e-12)) break;
+            for (int32_t b = target; b != h; b = gp[b]) {
+                int32_t e = gv[b], nb = b / g;
+                if (!plan_holds(slot_table, S, b, e)) {
+                    slot_table[(int64_t)b * S + plan_used(slot_table, S, b)] = e;
+                    on[(int64_t)e * N + nb] = 1;
+                    used[nb] += 1;
+                }
+                pl[(int64_t)e * G + gp[b]] -= mv;
+                pl[(int64_t)e * G + b] += mv;
+            }
+        }
+        free(gq); free(gp); free(gv); free(gs);
     }
 
     /* 3. co-activation replicas */

@@ -36,6 +36,10 @@
 //      below cap; with no such path, a slot swap moves a light expert from
 //      a full under-cap rank to h and part of h's heaviest expert into the
 //      freed slot.
+//   2b. Global repair: the same augmenting-path search over the ranks of all
+//      nodes, so that a node left above its ranks' caps passes work to
+//      replicas, or new replicas in free slots, on other nodes (a new
+//      replica makes its expert a member of that node); at most 4 G S moves.
 //   3. Co-activation replicas: while a node has a free slot, add the
 //      (e, n) with the largest positive gain (ties: larger w, smaller e,
 //      smaller n), with no planned work, on the node's rank with fewest
@@ -107,6 +111,7 @@ struct Planner {
     void local_search();
     void pack_node(int n);
     void repair_node(int n);
+    void repair_global();
     void coactivation_replicas();
 };
 
@@ -418,6 +423,63 @@ void Planner::repair_node(int n) {
     }
 }
 
+void Planner::repair_global() {
+    std::vector<double> load(G);
+    for (int r = 0; r < G; ++r) load[r] = rank_load(r);
+    std::vector<int> queue, parent(G, -1), via(G, -1);
+    std::vector<uint8_t> seen(G, 0);
+    for (int64_t moves = 0; moves < 4 * (int64_t)G * S; ++moves) {
+        int h = -1;
+        double hl = 0.0;
+        for (int r = 0; r < G; ++r)
+            if (h < 0 || load[r] > hl) {
+                h = r;
+                hl = load[r];
+            }
+        if (!(hl > cap)) return;
+
+        queue.assign(1, h);
+        std::fill(seen.begin(), seen.end(), 0);
+        seen[h] = 1;
+        int target = -1;
+        for (size_t qh = 0; qh < queue.size() && target < 0; ++qh) {
+            const int a = queue[qh];
+            std::vector<int32_t> ids = slots[a];
+            std::sort(ids.begin(), ids.end());
+            for (size_t t = 0; t < ids.size() && target < 0; ++t) {
+                const int e = ids[t];
+                if (!(pl[(size_t)e * G + a] > 0.0)) continue;
+                for (int b = 0; b < G && target < 0; ++b) {
+                    if (seen[b]) continue;
+                    if (!holds(b, e) && (int)slots[b].size() >= S) continue;
+                    seen[b] = 1;
+                    parent[b] = a;
+                    via[b] = e;
+                    queue.push_back(b);
+                    if (load[b] < cap) target = b;
+                }
+            }
+        }
+        if (target < 0) return;
+        double mv = std::min(hl - cap, cap - load[target]);
+        for (int b = target; b != h; b = parent[b])
+            mv = std::min(mv, pl[(size_t)via[b] * G + parent[b]]);
+        if (!(mv > cap * 1e-12)) return;
+        for (int b = target; b != h; b = parent[b]) {
+            const int e = via[b], a = parent[b], nb = b / g;
+            if (!holds(b, e)) {
+                slots[b].push_back(e);
+                if (!on[(size_t)e * N + nb]) join(e, nb);
+                used[nb] += 1;
+            }
+            pl[(size_t)e * G + a] -= mv;
+            pl[(size_t)e * G + b] += mv;
+        }
+        for (int b = target; b != h; b = parent[b]) load[b] = rank_load(b);
+        load[h] = rank_load(h);
+    }
+}
+
 void Planner::coactivation_replicas() {
     for (;;) {
         int be = -1, bn = -1;
@@ -516,6 +578,7 @@ extern "C" cobalt_status cobalt_plan_layout(int32_t N, int32_t gpn, int32_t E, i
         P.used[n] = 0;
         for (int i = 0; i < gpn; ++i) P.used[n] += (int64_t)P.slots[n * gpn + i].size();
     }
+    P.repair_global();
     P.coactivation_replicas();
 
     for (int r = 0; r < G; ++r)

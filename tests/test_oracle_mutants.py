@@ -83,6 +83,9 @@ MUTANTS = [
     ("Stage 1 ignores the work cap in the local search",
      "                if (!(wna <= node_cap || wna <= work[na])) continue;",
      "", ["test_oracle_plan.py"]),
+    ("Stage 1 skips the repair across nodes",
+     "for (int64_t moves = 0; moves < 4 * (int64_t)G * S; ++moves) {",
+     "for (int64_t moves = 0; moves < 0; ++moves) {", ["test_oracle_plan.py"]),
 ]
 
 

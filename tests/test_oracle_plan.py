@@ -179,3 +179,25 @@ def test_work_cap_overrides_co_activation():
     assert out[4], "a division within the cap exists: one heavy expert per node"
     assert loads.max() <= cap
     assert held.sum() == E and not (on[0] & on[1]).any()  # no spare slot: apart
+
+
+def test_a_full_node_passes_work_to_another_node():
+    """Two one-rank nodes with three slots, w = (7, 33, 5, 2), cap = 1.15 *
+    47 / 2 = 27.025. Expert 1 exceeds the cap, so it is split: placed first,
+    it fills node 0 to the cap and puts 5.975 on node 1. Experts 0 and 2 then
+    take node 1's two other slots, so expert 3 (work 2) can only go to node 0,
+    2 above the cap. No move inside a one-rank node helps. Only moving work of
+    expert 1 to its replica on node 1 restores the cap, and the repair moves
+    exactly the excess: 2."""
+    N, g, S, E = 2, 1, 3, 4
+    w = np.array([7, 33, 5, 2], np.float32)
+    c = np.zeros((E, E), np.float32)
+    c[1, 3] = c[3, 1] = 16.0
+    out = oracle.plan_layout(N, g, E, S, c, w, 0.15)
+    held, on, loads, cap = check_solution(N, g, E, S, c, w, 0.15, out)
+    table, owner, plan, obj, feasible = out
+    assert feasible and loads.max() <= cap * (1 + 1e-9)
+    assert sorted(int(e) for e in table[0] if e >= 0) == [1, 3]
+    assert sorted(int(e) for e in table[1] if e >= 0) == [0, 1, 2]
+    assert plan[1, 0] == np.float32(cap - 2.0) and plan[1, 1] == np.float32(33.0 - (cap - 2.0))
+    assert obj == 16.0
