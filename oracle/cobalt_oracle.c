@@ -777,12 +777,16 @@ done:
 /*    w_x, cap - load_u + w_x, l_eh,h) of eh moves to a new replica on u, */
 /*    if m > w_x. Stop when neither applies or a path move is below       */
 /*    cap 1e-12 (at most 4 g^2 S moves).                                  */
-/* 2b. Global repair. The same augmenting-path search over the ranks of  */
-/*    all nodes (ranks in increasing id), so that a node left above its   */
-/*    ranks' caps can pass work to replicas, or new replicas in free      */
-/*    slots, on other nodes: a new replica makes its expert a member of   */
-/*    that node. It stops when no rank exceeds cap, no rank below cap is  */
-/*    reachable, or a move is below cap 1e-12 (at most 4 G S moves).      */
+/* 2b. Global repair. While the most loaded rank h of all (ties: smaller) */
+/*    exceeds cap, the same breadth-first search over the ranks of all    */
+/*    nodes (increasing id), so that a node left above its ranks' caps    */
+/*    can pass work to another node. It searches first through ranks that */
+/*    already hold the path's expert, and only when that reaches no       */
+/*    target also through free slots (a new replica, which makes its     */
+/*    expert a member of that node). A target has room above cap 1e-12:   */
+/*    cap - load_t > cap 1e-12. It stops when no rank exceeds cap, no     */
+/*    target is reachable, or a move is below cap 1e-12 (at most 4 G S   */
+/*    moves).                                                             */
 /* 3. Co-activation replicas. While some (e, n) with e not on n, a free   */
 /*    slot on n and positive gain exists: add the one with the largest    */
 /*    gain (ties: larger w, smaller e, smaller n) on the rank of n with   */
@@ -1271,23 +1275,29 @@ int ref_plan_layout(int32_t N, int32_t g, int32_t E, int32_t S, const float* coa
                 }
             }
             if (!(hl > cap)) break;
-            int32_t qh = 0, qt = 0, target = -1;
-            for (int32_t r = 0; r < G; ++r) gs[r] = 0;
-            gq[qt++] = h;
-            gs[h] = 1;
-            while (qh < qt && target < 0) {
-                int32_t a = gq[qh++];
-                for (int32_t e = 0; e < E && target < 0; ++e) {
-                    if (!(pl[(int64_t)e * G + a] > 0.0)) continue;
-                    for (int32_t b = 0; b < G && target < 0; ++b) {
-                        if (gs[b]) continue;
-                        if (!plan_holds(slot_table, S, b, e) && plan_used(slot_table, S, b) >= S)
-                            continue;
-                        gs[b] = 1;
-                        gp[b] = a;
-                        gv[b] = e;
-                        gq[qt++] = b;
-                        if (plan_rank_load(pl, E, G, b) < cap) target = b;
+            /* phase 0: through held replicas only; phase 1: also new
+               replicas in free slots */
+            int32_t target = -1;
+            for (int32_t phase = 0; phase < 2 && target < 0; ++phase) {
+                int32_t qh = 0, qt = 0;
+                for (int32_t r = 0; r < G; ++r) gs[r] = 0;
+                gq[qt++] = h;
+                gs[h] = 1;
+                while (qh < qt && target < 0) {
+                    int32_t a = gq[qh++];
+                    for (int32_t e = 0; e < E && target < 0; ++e) {
+                        if (!(pl[(int64_t)e * G + a] > 0.0)) continue;
+                        for (int32_t b = 0; b < G && target < 0; ++b) {
+                            if (gs[b]) continue;
+                            if (!plan_holds(slot_table, S, b, e) &&
+                                (phase == 0 || plan_used(slot_table, S, b) >= S))
+                                continue;
+                            gs[b] = 1;
+                            gp[b] = a;
+                            gv[b] = e;
+                            gq[qt++] = b;
+                            if (cap - plan_rank_load(pl, E, G, b) > cap * 1e-12) target = b;
+                        }
                     }
                 }
             }

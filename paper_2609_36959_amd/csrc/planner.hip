@@ -38,8 +38,10 @@
 //      freed slot.
 //   2b. Global repair: the same augmenting-path search over the ranks of all
 //      nodes, so that a node left above its ranks' caps passes work to
-//      replicas, or new replicas in free slots, on other nodes (a new
-//      replica makes its expert a member of that node); at most 4 G S moves.
+//      another node: first through ranks that hold the path's expert, and
+//      only if that reaches no target through free slots too (a new replica
+//      makes its expert a member of that node). A target needs room above
+//      cap 1e-12; at most 4 G S moves.
 //   3. Co-activation replicas: while a node has a free slot, add the
 //      (e, n) with the largest positive gain (ties: larger w, smaller e,
 //      smaller n), with no planned work, on the node's rank with fewest
@@ -438,25 +440,28 @@ void Planner::repair_global() {
             }
         if (!(hl > cap)) return;
 
-        queue.assign(1, h);
-        std::fill(seen.begin(), seen.end(), 0);
-        seen[h] = 1;
+        // held replicas first; new replicas in free slots only if that fails
         int target = -1;
-        for (size_t qh = 0; qh < queue.size() && target < 0; ++qh) {
-            const int a = queue[qh];
-            std::vector<int32_t> ids = slots[a];
-            std::sort(ids.begin(), ids.end());
-            for (size_t t = 0; t < ids.size() && target < 0; ++t) {
-                const int e = ids[t];
-                if (!(pl[(size_t)e * G + a] > 0.0)) continue;
-                for (int b = 0; b < G && target < 0; ++b) {
-                    if (seen[b]) continue;
-                    if (!holds(b, e) && (int)slots[b].size() >= S) continue;
-                    seen[b] = 1;
-                    parent[b] = a;
-                    via[b] = e;
-                    queue.push_back(b);
-                    if (load[b] < cap) target = b;
+        for (int phase = 0; phase < 2 && target < 0; ++phase) {
+            queue.assign(1, h);
+            std::fill(seen.begin(), seen.end(), 0);
+            seen[h] = 1;
+            for (size_t qh = 0; qh < queue.size() && target < 0; ++qh) {
+                const int a = queue[qh];
+                std::vector<int32_t> ids = slots[a];
+                std::sort(ids.begin(), ids.end());
+                for (size_t t = 0; t < ids.size() && target < 0; ++t) {
+                    const int e = ids[t];
+                    if (!(pl[(size_t)e * G + a] > 0.0)) continue;
+                    for (int b = 0; b < G && target < 0; ++b) {
+                        if (seen[b]) continue;
+                        if (!holds(b, e) && (phase == 0 || (int)slots[b].size() >= S)) continue;
+                        seen[b] = 1;
+                        parent[b] = a;
+                        via[b] = e;
+                        queue.push_back(b);
+                        if (cap - load[b] > cap * 1e-12) target = b;
+                    }
                 }
             }
         }
