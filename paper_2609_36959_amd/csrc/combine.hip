@@ -4,13 +4,14 @@
 // order; slots whose row is outside [0, T*K) are skipped.
 //
 // fold_kernel: one workgroup per (token, 2 KiB column slice), one wave per
-// slot j (at least four waves). Wave j loads its row's slice (non-temporal,
-// two 16-byte chunks per lane) into LDS; after a barrier four waves fold the
-// K slices in slot order, two 32-bit words per thread, and store the slice
-// of y. Each wave has a single row to fetch, so many independent row loads
-// are in flight; on the T=131072, K=8, d=7168 workload this runs at
-// 6.3-6.4 TB/s, against 5.6 TB/s for combine_kernel. Folding with one wave
-// (two chunks per lane) instead holds the stage longer and costs 2 %.
+// slot j (at least two waves). Wave j loads its row's slice (non-temporal,
+// two 16-byte chunks per lane) into LDS; after a barrier two waves fold the
+// K slices in slot order, one 16-byte chunk (eight bf16 values) per thread,
+// and store the slice of y. Each wave has a single row to fetch, so many
+// independent row loads are in flight; on the T=131072, K=8, d=7168
+// workload this runs at 6.5-6.6 TB/s, against 5.6 TB/s for combine_kernel.
+// Four folding waves storing 8 bytes per thread took 3 % longer, and one
+// wave folding two chunks per lane holds the stage longer still.
 //
 // combine_kernel (other shapes): each wave takes one (token, 1 KiB slice)
 // and loads the chunks of all K rows itself, issuing every load before its
@@ -27,7 +28,8 @@ namespace cobalt {
 namespace {
 
 constexpr int kCombineWaves = 16;
-constexpr int kFoldWaves = 4;  // waves that fold a slice (128 chunks = 256 threads x 2 words)
+constexpr int kFoldWaves = 2;  // waves that fold or sum a staged slice (128 chunks, one per thread)
+constexpr int kNodeWaves = 4;  // least waves of node_fold_kernel; waves of node_sum_kernel
 
 __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
     const uint32_t u = __float_as_uint(f);
@@ -132,31 +134,33 @@ __global__ __launch_bounds__(kMaxK * 64) void fold_kernel(
         }
     }
     __syncthreads();
-    // kFoldWaves waves fold: thread i takes words 2i, 2i+1 of the slice
-    // (four bf16 values of chunk i / 2), summing the K slots in slot order
+    // kFoldWaves waves fold: thread i takes chunk i of the slice (eight bf16
+    // values), summing the K slots in slot order, and stores 16 bytes of y
     if (j >= kFoldWaves) return;
     const int i = threadIdx.x;
-    const int64_t c = (int64_t)g * 128 + (i >> 1);
+    const int64_t c = (int64_t)g * 128 + i;
     if (c >= nch) return;
-    const uint32_t* s32 = (const uint32_t*)stage;
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (int k = 0; k < K; ++k) {
         if (!valid[k]) continue;
         const float gk = gate[k];
-        const u32x2 v = *(const u32x2*)(s32 + k * 512 + 2 * i);
+        const u32x4 v = stage[k * 128 + i];
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
+        for (int q = 0; q < 4; ++q) {
             acc[2 * q] = __builtin_fmaf(gk, __uint_as_float(v[q] << 16), acc[2 * q]);
             acc[2 * q + 1] = __builtin_fmaf(gk, __uint_as_float(v[q] & 0xffff0000u), acc[2 * q + 1]);
         }
     }
-    u32x2 out;
+    u32x4 out;
 #pragma unroll
-    for (int q = 0; q < 2; ++q)
+    for (int q = 0; q < 4; ++q)
         out[q] = f32_to_bf16_rne(acc[2 * q]) | (f32_to_bf16_rne(acc[2 * q + 1]) << 16);
-    const int64_t w = ((int64_t)t * nch + (int64_t)g * 128) * 4 + 2 * i;  // word index in y
-    __builtin_nontemporal_store(out, (u32x2*)((uint32_t*)y + w));
-    if (kF32) *(float4*)(y32 + 2 * w) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    __builtin_nontemporal_store(out, y + (int64_t)t * nch + c);
+    if (kF32) {
+        float4* o = (float4*)(y32 + ((int64_t)t * nch + c) * 8);
+        o[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        o[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+    }
 }
 
 template <bool kF32, int GROUPS>
@@ -273,7 +277,7 @@ void launch_node_fold(const void* eo, const int32_t* pos, const int32_t* assigne
             return launch_node_fold<GROUPS - 1>(eo, pos, assigned, gates, node_pos, T, K, N, gpn,
                                                 nch, node_rows, partial, s);
     }
-    const int threads = std::max(K, kFoldWaves) * 64;
+    const int threads = std::max(K, kNodeWaves) * 64;
     for_token_ranges(T, groups * threads, [&](int64_t t0, int64_t n) {
         hipLaunchKernelGGL(node_fold_kernel<GROUPS>, dim3((unsigned)(n * groups)), dim3(threads),
                            (size_t)K * 128 * sizeof(u32x4), s, (const u32x4*)eo, pos + t0 * K,
@@ -285,13 +289,15 @@ void launch_node_fold(const void* eo, const int32_t* pos, const int32_t* assigne
 // Source side of the node-level combine: one workgroup of four waves per
 // (token, 2 KiB column slice). Wave j loads the node rows n = j, j + 4, ...
 // (SPW of them at most) that node_pos names for the token; after a barrier
-// the four waves sum the staged rows in increasing n, two 32-bit words per
-// thread, and store the slice of y. A token reaches only about half of the
-// nodes, so one wave per node would leave half the waves idle at the
-// barrier (1.91 ms against 1.65 ms on the T=131072, N=8, d=7168 workload).
+// two waves sum the staged rows in increasing n, one 16-byte chunk per
+// thread, and store the slice of y (four waves at 8 bytes per thread were
+// no faster). A token reaches only about
+// half of the nodes, so one loading wave per node would leave half the
+// waves idle at the barrier (1.91 ms against 1.65 ms on the T=131072, N=8,
+// d=7168 workload).
 // GROUPS as for node_fold_kernel.
 template <int GROUPS, int SPW>
-__global__ __launch_bounds__(kFoldWaves * 64) void node_sum_kernel(
+__global__ __launch_bounds__(kNodeWaves * 64) void node_sum_kernel(
     const u32x4* __restrict__ partial, const int32_t* __restrict__ node_pos, int N, int64_t nch,
     int64_t node_rows, int groups_rt, u32x4* __restrict__ y) {
     extern __shared__ u32x4 stage[];
@@ -312,7 +318,7 @@ __global__ __launch_bounds__(kFoldWaves * 64) void node_sum_kernel(
     bool ok[SPW];
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
-        const int n = j + kFoldWaves * i;
+        const int n = j + kNodeWaves * i;
         const int q = n < N ? node_pos[(int64_t)t * N + n] : -1;
         ok[i] = q >= 0 && q < node_rows;
         if (ok[i]) {
@@ -323,7 +329,7 @@ __global__ __launch_bounds__(kFoldWaves * 64) void node_sum_kernel(
     }
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
-        const int n = j + kFoldWaves * i;
+        const int n = j + kNodeWaves * i;
         if (n < N) {
             if (ok[i]) {
                 stage[n * 128 + lane] = v[i][0];
@@ -333,26 +339,26 @@ __global__ __launch_bounds__(kFoldWaves * 64) void node_sum_kernel(
         }
     }
     __syncthreads();
+    // kFoldWaves waves sum: thread i takes chunk i of the slice
+    if (j >= kFoldWaves) return;
     const int i = threadIdx.x;
-    const int64_t c = (int64_t)g * 128 + (i >> 1);
+    const int64_t c = (int64_t)g * 128 + i;
     if (c >= nch) return;
-    const uint32_t* s32 = (const uint32_t*)stage;
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (int n = 0; n < N; ++n) {
         if (!valid[n]) continue;
-        const u32x2 a = *(const u32x2*)(s32 + n * 512 + 2 * i);
+        const u32x4 a = stage[n * 128 + i];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
+        for (int h = 0; h < 4; ++h) {
             acc[2 * h] += __uint_as_float(a[h] << 16);
             acc[2 * h + 1] += __uint_as_float(a[h] & 0xffff0000u);
         }
     }
-    u32x2 out;
+    u32x4 out;
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < 4; ++h)
         out[h] = f32_to_bf16_rne(acc[2 * h]) | (f32_to_bf16_rne(acc[2 * h + 1]) << 16);
-    const int64_t w = ((int64_t)t * nch + (int64_t)g * 128) * 4 + 2 * i;
-    __builtin_nontemporal_store(out, (u32x2*)((uint32_t*)y + w));
+    __builtin_nontemporal_store(out, y + (int64_t)t * nch + c);
 }
 
 template <int GROUPS>
@@ -363,11 +369,11 @@ void launch_node_sum(const void* partial, const int32_t* node_pos, int64_t T, in
         if (groups != GROUPS)
             return launch_node_sum<GROUPS - 1>(partial, node_pos, T, N, nch, node_rows, y, s);
     }
-    const dim3 block(kFoldWaves * 64);
+    const dim3 block(kNodeWaves * 64);
     const size_t lds = (size_t)N * 128 * sizeof(u32x4);
-    for_token_ranges(T, groups * kFoldWaves * 64, [&](int64_t t0, int64_t n) {
+    for_token_ranges(T, groups * kNodeWaves * 64, [&](int64_t t0, int64_t n) {
         const dim3 grid((unsigned)(n * groups));
-        if (N <= 2 * kFoldWaves)
+        if (N <= 2 * kNodeWaves)
             hipLaunchKernelGGL((node_sum_kernel<GROUPS, 2>), grid, block, lds, s,
                                (const u32x4*)partial, node_pos + t0 * N, N, nch, node_rows,
                                (int)groups, (u32x4*)y + t0 * nch);

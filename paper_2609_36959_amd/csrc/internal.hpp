@@ -20,7 +20,6 @@ constexpr int kMaxE = 4096;
 // 16-byte vector: eight bf16 values, the unit of every row copy.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // 8-byte vector: four bf16 values.
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 struct DeviceLayout {
     int device;
