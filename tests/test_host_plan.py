@@ -86,3 +86,24 @@ def test_library_rejects_what_the_oracle_rejects():
     edge = z.copy()
     edge[0, 1] = edge[1, 0] = 2.0**28
     same(2, 2, 8, 2, edge, one, 0.1)
+
+
+def tight_instance(seed):
+    """Zipf(1.2) work on 4 x 4 ranks with one spare slot per rank: the node
+    fill of step 1 leaves ranks above the cap that only the repair across
+    nodes can bring back."""
+    rng = np.random.default_rng(100 + seed)
+    N, g = 4, 4
+    E = 48 + 8 * (seed % 3)
+    S = -(-E // (N * g)) + 1
+    w = ((1.0 / np.arange(1, E + 1) ** 1.2)[rng.permutation(E)] * 1000).astype(np.float32)
+    c = (rng.random((E, E)) * 10).astype(np.float32)
+    c[rng.random((E, E)) > 0.3] = 0
+    c = np.triu(c, 1)
+    return N, g, E, S, c + c.T, w
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_tight_slots_and_the_repair_across_nodes(seed):
+    N, g, E, S, c, w = tight_instance(seed)
+    same(N, g, E, S, c, w, 0.15)

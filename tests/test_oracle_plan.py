@@ -201,3 +201,24 @@ def test_a_full_node_passes_work_to_another_node():
     assert sorted(int(e) for e in table[1] if e >= 0) == [0, 1, 2]
     assert plan[1, 0] == np.float32(cap - 2.0) and plan[1, 1] == np.float32(33.0 - (cap - 2.0))
     assert obj == 16.0
+
+
+def test_tight_slots_meet_the_cap():
+    """Zipf(1.2) work on 4 x 4 ranks with one spare slot per rank (E = 48,
+    56, 64). The repair across nodes brings every plan but one within the
+    cap; each plan that says so must satisfy Eq. 3's constraints."""
+    within = 0
+    for seed in range(12):
+        rng = np.random.default_rng(100 + seed)
+        N, g = 4, 4
+        E = 48 + 8 * (seed % 3)
+        S = -(-E // (N * g)) + 1
+        w = ((1.0 / np.arange(1, E + 1) ** 1.2)[rng.permutation(E)] * 1000).astype(np.float32)
+        c = (rng.random((E, E)) * 10).astype(np.float32)
+        c[rng.random((E, E)) > 0.3] = 0
+        c = np.triu(c, 1)
+        c = c + c.T
+        out = oracle.plan_layout(N, g, E, S, c, w, 0.15)
+        check_solution(N, g, E, S, c, w, 0.15, out)
+        within += bool(out[4])
+    assert within >= 11
