@@ -791,6 +791,11 @@ done:
 /*    slot on n and positive gain exists: add the one with the largest    */
 /*    gain (ties: larger w, smaller e, smaller n) on the rank of n with   */
 /*    fewest replicas (ties: smaller), with no planned work.              */
+/* Retries. If the plan exceeds the cap, steps 1 to 3 run again with the */
+/* node work bound of step 1 and its local search lowered to f g cap,     */
+/* f = 0.98, 0.95, 0.90 in turn, which leaves work slack on every node    */
+/* for steps 2 and 2b. The first plan within the cap is returned; if none */
+/* is (or a retry finds no slot for some expert), the plan with f = 1.    */
 /* owner[e]: the rank with the most planned work for e (ties: smaller).   */
 /* plan [E][G]: planned work l_er (fp32 of the double sums); objective:    */
 /* the quantised objective / 256; feasible: every rank's planned work is   */
@@ -848,9 +853,9 @@ static double plan_rank_load(const double* pl, int32_t E, int32_t G, int32_t r)
     return l;
 }
 
-int ref_plan_layout(int32_t N, int32_t g, int32_t E, int32_t S, const float* coact_ema,
-                    const float* count_ema, float eps, int32_t* slot_table, int32_t* owner,
-                    float* plan, double* objective, int32_t* feasible)
+static int plan_once(int32_t N, int32_t g, int32_t E, int32_t S, const float* coact_ema,
+                     const float* count_ema, float eps, double node_frac, int32_t* slot_table,
+                     int32_t* owner, float* plan, double* objective, int32_t* feasible)
 {
     if (N < 1 || N > 16 || g < 1 || g > 32 || E < 1 || E > 4096 || S < 1) return REF_EINVAL;
     if (!(eps >= 0.0f) || isinf(eps)) return REF_EINVAL;
@@ -891,7 +896,7 @@ int ref_plan_layout(int32_t N, int32_t g, int32_t E, int32_t S, const float* coa
     double W = 0.0;
     for (int32_t e = 0; e < E; ++e) W += (double)count_ema[e];
     double cap = (1.0 + (double)eps) * W / (double)G;
-    double node_cap = (double)g * cap;
+    double node_cap = (double)g * cap * node_frac;
     int64_t all_slots = (int64_t)g * S;
     /* slots each node keeps free through step 1 for the repair of step 2 */
     int64_t total_need = 0;
@@ -1380,4 +1385,43 @@ done:
     free(q); free(on); free(share); free(pieces); free(order); free(used); free(work); free(pl);
     free(items); free(rload); free(dest);
     return rc;
+}
+
+int ref_plan_layout(int32_t N, int32_t g, int32_t E, int32_t S, const float* coact_ema,
+                    const float* count_ema, float eps, int32_t* slot_table, int32_t* owner,
+                    float* plan, double* objective, int32_t* feasible)
+{
+    /* node fill fractions of step 1 and 1b after the first */
+    static const double retry[3] = { 0.98, 0.95, 0.90 };
+    int32_t ok = 0;
+    int rc = plan_once(N, g, E, S, coact_ema, count_ema, eps, 1.0, slot_table, owner, plan,
+                       objective, &ok);
+    if (rc != REF_OK || ok) {
+        if (rc == REF_OK && feasible) *feasible = ok;
+        return rc;
+    }
+    int32_t G = N * g;
+    int32_t* t2 = (int32_t*)malloc((size_t)G * S * sizeof(int32_t));
+    int32_t* o2 = (int32_t*)malloc((size_t)E * sizeof(int32_t));
+    float* p2 = (float*)malloc((size_t)E * G * sizeof(float));
+    if (!t2 || !o2 || !p2) {
+        free(t2); free(o2); free(p2);
+        return REF_EINVAL;
+    }
+    for (int k = 0; k < 3 && !ok; ++k) {
+        double obj2 = 0.0;
+        int32_t ok2 = 0;
+        if (plan_once(N, g, E, S, coact_ema, count_ema, eps, retry[k], t2, o2, p2, &obj2, &ok2) !=
+                REF_OK ||
+            !ok2)
+            continue;
+        memcpy(slot_table, t2, (size_t)G * S * sizeof(int32_t));
+        memcpy(owner, o2, (size_t)E * sizeof(int32_t));
+        if (plan) memcpy(plan, p2, (size_t)E * G * sizeof(float));
+        if (objective) *objective = obj2;
+        ok = 1;
+    }
+    free(t2); free(o2); free(p2);
+    if (feasible) *feasible = ok;
+    return REF_OK;
 }

@@ -47,6 +47,10 @@
 //      smaller n), with no planned work, on the node's rank with fewest
 //      replicas (ties: smaller).
 //   owner[e]: the rank with the most planned work for e (ties: smaller).
+//   Retries: a plan above the cap is made again with the node work bound of
+//   steps 1 and 1b at f g cap, f = 0.98, 0.95, 0.90 in turn (slack on every
+//   node for steps 2 and 2b); the first plan within the cap is returned, and
+//   if none is, the plan with f = 1.
 //
 // Rank loads are always summed over the rank's experts in increasing id, so
 // every floating-point decision is reproducible.
@@ -513,32 +517,12 @@ void Planner::coactivation_replicas() {
     }
 }
 
-}  // namespace
-}  // namespace cobalt
-
-using namespace cobalt;
-
-extern "C" cobalt_status cobalt_plan_layout(int32_t N, int32_t gpn, int32_t E, int32_t S,
-                                            const float* coact_ema, const float* count_ema,
-                                            float eps, int32_t* slot_table, int32_t* owner,
-                                            float* plan, double* objective,
-                                            int32_t* feasible) {
-    if (!coact_ema || !count_ema || !slot_table || !owner) return COBALT_EINVAL;
-    if (N < 1 || N > kMaxN || gpn < 1 || gpn > kMaxGpn || E < 1 || E > kMaxE || S < 1)
-        return COBALT_EINVAL;
-    if (!(eps >= 0.0f) || std::isinf(eps)) return COBALT_EINVAL;
+// One run of the steps with the node work bound of step 1 and its local
+// search at node_frac * g * cap. Arguments are checked by the caller.
+cobalt_status plan_once(int32_t N, int32_t gpn, int32_t E, int32_t S, const float* coact_ema,
+                        const float* count_ema, float eps, double node_frac, int32_t* slot_table,
+                        int32_t* owner, float* plan, double* objective, int32_t* feasible) {
     const int G = N * gpn;
-    if ((int64_t)G * S < E) return COBALT_EINVAL;
-    for (int e = 0; e < E; ++e)
-        if (!(count_ema[e] >= 0.0f) || std::isinf(count_ema[e])) return COBALT_EDATA;
-    for (int i = 0; i < E; ++i)
-        for (int j = i + 1; j < E; ++j) {
-            const float c = coact_ema[(size_t)i * E + j];
-            // q <= 2^36: the objective, at most kMaxN nodes x E(E-1)/2 < 2^23
-            // pairs of them, stays below 2^63
-            if (!(c >= 0.0f) || !(c <= 268435456.0f)) return COBALT_EDATA;  // 2^28
-        }
-
     Planner P;
     P.N = N;
     P.g = gpn;
@@ -562,7 +546,7 @@ extern "C" cobalt_status cobalt_plan_layout(int32_t N, int32_t gpn, int32_t E, i
     double W = 0.0;
     for (int e = 0; e < E; ++e) W += (double)count_ema[e];
     P.cap = (1.0 + (double)eps) * W / (double)G;
-    P.node_cap = (double)gpn * P.cap;
+    P.node_cap = (double)gpn * P.cap * node_frac;
     P.all_slots = (int64_t)gpn * S;
     int64_t total_need = 0;
     for (int e = 0; e < E; ++e) total_need += P.need((double)count_ema[e]);
@@ -615,3 +599,58 @@ extern "C" cobalt_status cobalt_plan_layout(int32_t N, int32_t gpn, int32_t E, i
     }
     return COBALT_OK;
 }
+
+}  // namespace
+}  // namespace cobalt
+
+using namespace cobalt;
+
+extern "C" cobalt_status cobalt_plan_layout(int32_t N, int32_t gpn, int32_t E, int32_t S,
+                                            const float* coact_ema, const float* count_ema,
+                                            float eps, int32_t* slot_table, int32_t* owner,
+                                            float* plan, double* objective,
+                                            int32_t* feasible) {
+    if (!coact_ema || !count_ema || !slot_table || !owner) return COBALT_EINVAL;
+    if (N < 1 || N > kMaxN || gpn < 1 || gpn > kMaxGpn || E < 1 || E > kMaxE || S < 1)
+        return COBALT_EINVAL;
+    if (!(eps >= 0.0f) || std::isinf(eps)) return COBALT_EINVAL;
+    const int G = N * gpn;
+    if ((int64_t)G * S < E) return COBALT_EINVAL;
+    for (int e = 0; e < E; ++e)
+        if (!(count_ema[e] >= 0.0f) || std::isinf(count_ema[e])) return COBALT_EDATA;
+    for (int i = 0; i < E; ++i)
+        for (int j = i + 1; j < E; ++j) {
+            const float c = coact_ema[(size_t)i * E + j];
+            // q <= 2^36: the objective, at most kMaxN nodes x E(E-1)/2 < 2^23
+            // pairs of them, stays below 2^63
+            if (!(c >= 0.0f) || !(c <= 268435456.0f)) return COBALT_EDATA;  // 2^28
+        }
+
+    int32_t ok = 0;
+    cobalt_status st = plan_once(N, gpn, E, S, coact_ema, count_ema, eps, 1.0, slot_table, owner,
+                                 plan, objective, &ok);
+    if (st != COBALT_OK || ok) {
+        if (st == COBALT_OK && feasible) *feasible = ok;
+        return st;
+    }
+    // above the cap: retry with slack left on every node by steps 1 and 1b
+    static const double retry[3] = {0.98, 0.95, 0.90};
+    std::vector<int32_t> t2((size_t)G * S), o2(E);
+    std::vector<float> p2((size_t)E * G);
+    for (int k = 0; k < 3 && !ok; ++k) {
+        double obj2 = 0.0;
+        int32_t ok2 = 0;
+        if (plan_once(N, gpn, E, S, coact_ema, count_ema, eps, retry[k], t2.data(), o2.data(),
+                      p2.data(), &obj2, &ok2) != COBALT_OK ||
+            !ok2)
+            continue;
+        std::copy(t2.begin(), t2.end(), slot_table);
+        std::copy(o2.begin(), o2.end(), owner);
+        if (plan) std::copy(p2.begin(), p2.end(), plan);
+        if (objective) *objective = obj2;
+        ok = 1;
+    }
+    if (feasible) *feasible = ok;
+    return COBALT_OK;
+}
+

@@ -86,6 +86,9 @@ MUTANTS = [
     ("Stage 1 skips the repair across nodes",
      "for (int64_t moves = 0; moves < 4 * (int64_t)G * S; ++moves) {",
      "for (int64_t moves = 0; moves < 0; ++moves) {", ["test_oracle_plan.py"]),
+    ("Stage 1 skips the retries with node slack",
+     "for (int k = 0; k < 3 && !ok; ++k) {", "for (int k = 0; k < 0 && !ok; ++k) {",
+     ["test_oracle_plan_milp.py"]),
 ]
 
 

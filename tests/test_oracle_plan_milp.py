@@ -93,3 +93,31 @@ def test_heuristic_is_within_the_exact_bound(N, g, E, seed):
     if feasible:
         assert obj <= bound * (1 + 1e-6) + 1e-6
     assert obj >= 0.7 * best
+
+
+def test_a_tight_instance_is_brought_within_the_cap():
+    """Three nodes of two ranks with two slots each hold nine experts; expert
+    0 (work 273) needs more than two ranks at cap = 1.15 * 485 / 6 = 92.958.
+    The MILP finds a plan within the cap, so Eq. 3 is feasible here. Step 1
+    fills node 0 with expert 0 up to g cap. The repairs inside and across
+    nodes then find no rank with room and a free slot. Only the retry with
+    work slack on every node reaches the cap."""
+    N, g, S, E = 3, 2, 2, 9
+    w = np.array([273, 32, 5, 54, 8, 7, 19, 64, 23], np.float32)
+    c = np.zeros((E, E), np.float32)
+    for i, j, v in [(0, 1, 18), (0, 2, 5), (0, 6, 12), (1, 3, 7), (1, 6, 11), (1, 7, 19),
+                    (2, 3, 4), (2, 8, 9), (4, 5, 16), (4, 6, 1)]:
+        c[i, j] = c[j, i] = v
+    best, bound = eq3_milp(N, g, E, S, c, w, 0.15, time_limit=20)
+    table, owner, plan, obj, feasible = oracle.plan_layout(N, g, E, S, c, w, 0.15)
+    assert feasible and obj <= bound * (1 + 1e-6) + 1e-6
+    cap = 1.15 * float(w.astype(np.float64).sum()) / (N * g)
+    loads = plan.astype(np.float64).sum(0)
+    assert loads.max() <= cap * (1 + 1e-6)
+    held = np.zeros((E, N * g), bool)
+    for r in range(N * g):
+        ids = [int(e) for e in table[r] if e >= 0]
+        assert len(ids) == len(set(ids)) and len(ids) <= S
+        held[ids, r] = True
+    assert held.any(1).all() and not plan[~held].any()
+    assert np.allclose(plan.astype(np.float64).sum(1), w, rtol=1e-5)
