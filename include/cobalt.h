@@ -306,9 +306,11 @@ cobalt_status cobalt_intra_node_rebalance(int32_t N, int32_t gpus_per_node, int3
  * paper solves this as a MILP; this is a deterministic greedy heuristic for
  * the same objective and constraints (work placement on nodes by longest
  * processing time, moves and swaps that raise the objective, rank packing
- * with augmenting-path repair of the work division, then replicas that
- * raise the objective in the remaining slots). Pair weights are quantised
- * to 1/256 so that every comparison of gains is exact.
+ * with augmenting-path repair of the work division inside each node and
+ * then across nodes, then replicas that raise the objective in the
+ * remaining slots; a plan above the cap is made again with work slack left
+ * on every node). Pair weights are quantised to 1/256 so that every
+ * comparison of gains is exact.
  *
  * host_coact_ema [E][E] fp32 in: c_ij (EMA of co-activation counts; only
  *   i < j is read; finite, >= 0, <= 2^28, so that every integer sum of the
