@@ -200,6 +200,66 @@ def stage2_demo(st, torch, B, W):
             "imbalance_after": float(after.max() / mean), "host_ms": host_ms}
 
 
+def drift_with_stage2(st, w, routes, first_layout, replan, fns, torch, B, decay=0.9):
+    """The drift cycle once more, untimed, with Stage 2 (Section 3.2) after
+    every step: the step's per-replica loads w_er fold into a GPU EMA
+    (started from the first step's counts, and from the planned division
+    w'_er after the Stage-1 re-plan), and the host rebalancing turns the EMA
+    into the layout of the next step. Reports Eq. 1's V and the rank-load
+    imbalance of each step's assignment, averaged before and after the
+    re-plan."""
+    import numpy as np
+    st.set_layout(*first_layout)
+    st.coact.zero_()
+    st.count.zero_()
+    st.replica_load.zero_()
+    rema = torch.zeros(w.E, w.G, dtype=torch.float32, device=st.device)
+    per_step, host_ms = [], []
+    for s_ in range(w.steps):
+        flags = B.EMA_CLEAR
+        if s_ == 0:
+            flags |= B.EMA_INIT
+        if s_ == w.swap_step:
+            torch.cuda.synchronize()
+            rema.copy_(torch.from_numpy(replan(s_)))
+        st.topk, st.gates = routes[s_]
+        st.step = s_
+        for f in fns[:-2]:  # statistics, EMA and assignment
+            f()
+        rn32 = st.remote.to(torch.int32) & 0xFFFF
+        V = sum(((rn32 >> n) & 1).sum().item() for n in range(w.N))
+        per_rank = torch.bincount(st.assigned.flatten().long(), minlength=w.G).float()
+        per_step.append((int(V), float(per_rank.max() / per_rank.mean())))
+        st.load()
+        B.cobalt_count_ema(st.replica_load, decay, flags, rema)
+        rl = rema.cpu().numpy()
+        t0 = time.perf_counter()
+        table, owner, _ = B.cobalt_intra_node_rebalance(w.N, w.g, w.E, st.table.shape[1],
+                                                        st.table, st.owner, rl)
+        host_ms.append((time.perf_counter() - t0) * 1e3)
+        # the EMA follows the replicas: Algorithm 1 splits a node's tasks of
+        # an expert evenly over its replicas there, so each new replica gets
+        # the node's total for the expert divided by their number
+        held_old = np.zeros((w.E, w.G), bool)
+        held_new = np.zeros((w.E, w.G), bool)
+        for r in range(w.G):
+            held_old[[e for e in st.table[r] if e >= 0], r] = True
+            held_new[[e for e in table[r] if e >= 0], r] = True
+        node_sum = np.where(held_old, rl, 0.0).reshape(w.E, w.N, w.g).sum(2)
+        k_new = held_new.reshape(w.E, w.N, w.g).sum(2)
+        share = np.divide(node_sum, k_new, out=np.zeros_like(node_sum), where=k_new > 0)
+        remap = np.where(held_new, np.repeat(share, w.g, axis=1), 0.0).astype(np.float32)
+        rema.copy_(torch.from_numpy(remap))
+        st.set_layout(table, owner)
+    before, after = per_step[:w.swap_step], per_step[w.swap_step:]
+    return {"ema_decay": decay,
+            "mean_V_before": sum(v for v, _ in before) / len(before),
+            "mean_V_after": sum(v for v, _ in after) / len(after),
+            "mean_imbalance_before": sum(i for _, i in before) / len(before),
+            "mean_imbalance_after": sum(i for _, i in after) / len(after),
+            "rebalance_host_ms": sum(host_ms) / len(host_ms)}
+
+
 def stage1_demo(st, torch, B):
     """Periodic global planning (Section 3.2, Stage 1) from the EMAs the GPU
     keeps: the host planner turns ema_coact / ema_count into a layout, and
@@ -356,10 +416,11 @@ def main():
         the workload's hot-order recipe on the accumulated expert counts."""
         if planner:
             tp = time.perf_counter()
-            table, owner, _, obj, within = B.cobalt_plan_layout(
+            table, owner, plan, obj, within = B.cobalt_plan_layout(
                 w.N, w.g, w.E, w.S, st.ema_coact, st.ema_count, 0.15)
             plan_info.append(((time.perf_counter() - tp) * 1e3, obj, within))
             st.set_layout(table, owner)
+            return plan
         else:
             counts = st.count.cpu().numpy().view("uint32").astype("int64")
             hot = sorted(range(w.E), key=lambda e: (-counts[e], e))
@@ -484,6 +545,7 @@ def main():
             result["replan"].update({
                 "planner_host_ms": sum(p[0] for p in plan_info) / len(plan_info),
                 "objective": plan_info[-1][1], "plan_within_cap": plan_info[-1][2]})
+
     if not drift and not args.no_graph:
         # the same four calls captured once as a HIP graph and replayed
         g = torch.cuda.CUDAGraph()
@@ -608,6 +670,10 @@ def main():
     result["routing"]["stage1_plan"] = stage1_demo(st, torch, B)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(st, args.cpu_sample_tokens, torch, W, PL)
+    if planner:
+        # last, since it leaves another layout and assignment behind
+        result["replan"]["with_stage2_each_step"] = drift_with_stage2(
+            st, w, routes, first_layout, replan, fns, torch, B)
     st.close()
     print(json.dumps(result), flush=True)
 
