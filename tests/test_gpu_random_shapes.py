@@ -3,6 +3,8 @@ node-deduplicated dispatch and node-level combine, on configurations drawn
 across the ABI's ranges (1-16 nodes, 1-32 GPUs per node up to 512 ranks,
 E up to 4096, K 1-16, 8-4096-element rows, null, contiguous-length and
 ragged sources), each checked bit for bit against the oracle."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -38,7 +40,9 @@ def _configs(n, seed=2024):
     return out
 
 
-CONFIGS = _configs(24)
+# COBALT_RANDOM_SHAPES=n,seed draws another set (default: 24 shapes, seed 2024)
+_n, _seed = (int(v) for v in os.environ.get("COBALT_RANDOM_SHAPES", "24,2024").split(","))
+CONFIGS = _configs(_n, _seed)
 
 
 @pytest.fixture(scope="module", autouse=True)
