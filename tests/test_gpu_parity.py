@@ -321,3 +321,28 @@ def test_path_matches_oracle_over_seeds(seed, name, T, d):
     for mode in (0, 1):
         check_against_oracle(w, seed, topk.numpy(), gates.numpy(), table, owner, step=seed,
                              mode=mode)
+
+
+def test_every_call_is_deterministic_over_ten_repeats():
+    """Ten repeats of the four calls (fresh statistics each time) give the
+    same bits: a race in the look-back scan, the statistics or the scatter
+    would show up as a difference."""
+    w = W.with_sizes(W.WORKLOADS["colocate-e256"], T=64 * 300 + 17, d=1024)
+    print("determinism case colocate-e256 T=19217 d=1024", flush=True)
+    st = PL.RoutingStep(w, seed=7, device="cuda", route_device="cpu",
+                        src=W.ragged_src(w.T, w.G, seed=7))
+    ref = None
+    for rep in range(10):
+        st.coact.zero_()
+        st.count.zero_()
+        st.run()
+        torch.cuda.synchronize()
+        got = [u32(st.coact), u32(st.count), st.assigned.cpu().numpy(), st.remote.cpu().numpy(),
+               st.counts.cpu().numpy(), st.offsets.cpu().numpy(), st.pos.cpu().numpy(),
+               PL.bf16_bits(st.packed), PL.bf16_bits(st.y)]
+        if ref is None:
+            ref = got
+        else:
+            for a, b in zip(ref, got):
+                assert np.array_equal(a, b), f"repeat {rep} differs"
+    st.close()
