@@ -92,6 +92,7 @@ cobalt_status cobalt_layout_tables(cobalt_layout_t layout, uint32_t* host_node_m
  * across calls (and steps) until the caller clears them. With distinct
  * experts per token coact is symmetric with a zero diagonal and row sums
  * (K-1) * expert_count.
+ * K > E is rejected with COBALT_EINVAL (a token's experts are distinct).
  * workspace: device scratch of at least cobalt_coact_stats_workspace_bytes(
  *   T, K, E) bytes (partial histograms, about 4 * min(64, T/2048) * E(E-1)/2
  *   bytes), 256-byte aligned, owned by the caller; contents on entry are
@@ -120,6 +121,7 @@ cobalt_status cobalt_coact_stats(const int32_t* topk_idx, int64_t T, int32_t K, 
  *   holding it, then every task draws one rank of its node holding the
  *   expert. No load cap is applied.
  * mode 1 = owner-only baseline: every task runs on its expert's owner rank.
+ * K above the layout's E is rejected with COBALT_EINVAL.
  * Draws are counter-based: with sm(z) the SplitMix64 output for state z
  * (Steele, Lea & Flood 2014), key = sm(sm(seed) ^ step),
  * h = sm(key ^ (p << 1 | s)) for pair p and draw s (0 = node, 1 = rank),

@@ -186,6 +186,7 @@ extern "C" cobalt_status cobalt_coact_stats(const int32_t* topk, int64_t T, int3
                                             uint32_t* coact, uint32_t* count, void* ws,
                                             size_t ws_bytes, void* stream) {
     if (T < 0 || K < 1 || K > kMaxK || E < 1 || E > kMaxE || !coact || !ws) return COBALT_EINVAL;
+    if (K > E) return COBALT_EINVAL;  // a token's K experts are distinct
     if (T > 0 && !topk) return COBALT_EINVAL;
     if (((uintptr_t)ws & 255u) != 0) return COBALT_EINVAL;
     if (T * K >= (int64_t(1) << 31)) return COBALT_EUNSUPPORTED;
@@ -199,6 +200,7 @@ extern "C" cobalt_status cobalt_assign(cobalt_layout_t L, const int32_t* topk,
                                        uint64_t step, int32_t mode, int32_t* out,
                                        uint16_t* remote, void* stream) {
     if (!L || T < 0 || K < 1 || K > kMaxK || (mode != 0 && mode != 1)) return COBALT_EINVAL;
+    if (K > L->d.E) return COBALT_EINVAL;  // a token's K experts are distinct
     if (T > 0 && (!topk || !out)) return COBALT_EINVAL;
     if (T * K >= (int64_t(1) << 31)) return COBALT_EUNSUPPORTED;
     if (!src && T % L->d.G != 0) return COBALT_EINVAL;

@@ -83,6 +83,8 @@ def test_argument_checks_reject_before_device_work():
     assert L.cobalt_coact_stats(fake, 10, 2, 16, fake, None, fake, 16, None) == EINVAL
     assert L.cobalt_coact_stats(fake, 1 << 28, 8, 16, fake, None, fake, big,
                                 None) == EUNSUPPORTED
+    # K > E: a token cannot select K distinct experts
+    assert L.cobalt_coact_stats(fake, 10, 5, 4, fake, None, fake, big, None) == EINVAL
     # assign: null layout, bad mode
     assert L.cobalt_assign(None, fake, None, 8, 2, 0, 0, 0, fake, None, None) == EINVAL
     assert L.cobalt_assign(fake, fake, None, 8, 2, 0, 0, 7, fake, None, None) == EINVAL

@@ -133,3 +133,20 @@ def test_invalid_ids_ranks_and_sources(src_kind):
         rt = rtok.cpu().numpy()[:rows]
         assert np.array_equal(rt[q[reach]], np.nonzero(reach)[0])
     B.cobalt_layout_destroy(L)
+
+
+def test_assign_rejects_k_above_the_layouts_experts():
+    """A token selects K distinct experts, so K > E is refused on the host
+    and nothing is written."""
+    N, g, E, S = 2, 2, 4, 2
+    table = np.array([[0, 1], [1, 2], [2, 3], [3, 0]], np.int32)
+    L = B.cobalt_layout_create(N, g, E, S, table)
+    T, K = 8, 5
+    topk = torch.zeros(T, K, dtype=torch.int32, device="cuda")
+    out = torch.full((T, K), -3, dtype=torch.int32, device="cuda")
+    with pytest.raises(B.CobaltError) as e:
+        B.cobalt_assign(L, topk, None, 0, 0, 0, out)
+    assert e.value.status == 1  # COBALT_EINVAL
+    torch.cuda.synchronize()
+    assert bool((out == -3).all().item())
+    B.cobalt_layout_destroy(L)
