@@ -164,6 +164,34 @@ cobalt_status cobalt_dispatch_pack(const int32_t* assigned_rank, const int32_t* 
                                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Step 3 without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc and its like).
+ *
+ * Same arguments, outputs and errors as cobalt_dispatch_pack, less the
+ * workspace: its place is taken by a fixed scratch array of
+ * COBALT_DISPATCH_NOALLOC_SCRATCH_BYTES bytes in the library's device
+ * memory. Each GPU the library runs on holds its own copy from when the
+ * library's code is loaded there until the process ends. The call allocates
+ * nothing; its first call on a device only looks up that device's copy.
+ * Returns COBALT_EUNSUPPORTED, before anything is enqueued, when
+ * cobalt_dispatch_workspace_bytes(T, K, G) exceeds the array (with G = 64
+ * that is above 33 486 848 pairs T*K; with G = 512, above 3 667 968).
+ * Every call on one GPU uses that GPU's one array, and the array keeps what
+ * the last call left in it (each call re-initialises what it reads), so
+ * calls that may overlap on one GPU (different streams, or host threads
+ * without ordering) race and give wrong results: issue them on one stream,
+ * or order them. Calls on different GPUs do not interact.
+ * ---------------------------------------------------------------------- */
+#define COBALT_DISPATCH_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)
+
+cobalt_status cobalt_dispatch_pack_noalloc(const int32_t* assigned_rank, const int32_t* src_rank,
+                                           int64_t T, int32_t K, int32_t G,
+                                           const void* x, int64_t d,
+                                           int32_t* send_counts, int64_t* send_offsets,
+                                           int32_t* pos, void* packed, void* stream);
+
+/* ------------------------------------------------------------------------
  * Step 3': node-deduplicated dispatch layout and pack (Section 1 and
  * Section 3.1, Eq. 1: a token crosses to a node once, however many ranks
  * there need it, and is then forwarded inside the node).

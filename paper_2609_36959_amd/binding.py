@@ -59,6 +59,8 @@ def lib() -> ctypes.CDLL:
         "cobalt_dispatch_workspace_bytes": ([i64, i32, i32], sz),
         "cobalt_dispatch_pack": ([P, P, i64, i32, i32, P, i64, P, P, P, P, P, sz, P],
                                  ctypes.c_int),
+        "cobalt_dispatch_pack_noalloc": ([P, P, i64, i32, i32, P, i64, P, P, P, P, P],
+                                         ctypes.c_int),
         "cobalt_node_dispatch_workspace_bytes": ([i64, i32, i32], sz),
         "cobalt_node_dispatch_pack": ([P, P, i64, i32, i32, i32, P, i64, P, P, P, P, P, P, P, sz,
                                        P], ctypes.c_int),
@@ -204,6 +206,28 @@ def cobalt_dispatch_pack(assigned_rank: torch.Tensor, src_rank: Optional[torch.T
           _dev(packed, "packed", BF16, None if packed is None else (T * K, d)),
           _dev(workspace, "workspace", WS),
           workspace.numel() * workspace.element_size(), _stream(stream))
+
+
+DISPATCH_NOALLOC_SCRATCH_BYTES = 8 << 20  # COBALT_DISPATCH_NOALLOC_SCRATCH_BYTES
+
+
+def cobalt_dispatch_pack_noalloc(assigned_rank: torch.Tensor, src_rank: Optional[torch.Tensor],
+                                 G: int, x: Optional[torch.Tensor], send_counts: torch.Tensor,
+                                 send_offsets: torch.Tensor, pos: torch.Tensor,
+                                 packed: Optional[torch.Tensor], stream=None) -> None:
+    """cobalt_dispatch_pack with the library's fixed scratch in place of a
+    workspace; calls that may overlap on one GPU must not be issued."""
+    T, K = assigned_rank.shape
+    d = 0 if x is None else x.shape[1]
+    if x is not None:
+        _dev(x, "x", BF16, (T, d))
+    _call("cobalt_dispatch_pack_noalloc", _dev(assigned_rank, "assigned_rank", I32),
+          _dev(src_rank, "src_rank", I32, (T,)), T, K, G, _dev(x, "x", BF16), d,
+          _dev(send_counts, "send_counts", I32, (G, G)),
+          _dev(send_offsets, "send_offsets", I64, (G * G + 1,)),
+          _dev(pos, "pos", I32, (T, K)),
+          _dev(packed, "packed", BF16, None if packed is None else (T * K, d)),
+          _stream(stream))
 
 
 def cobalt_node_dispatch_workspace_bytes(T: int, N: int, gpus_per_node: int) -> int:

@@ -215,20 +215,47 @@ extern "C" size_t cobalt_dispatch_workspace_bytes(int64_t T, int32_t K, int32_t 
     return dispatch_workspace_bytes(T, K, G);
 }
 
+// Host checks shared by both dispatch entry points (all but the workspace).
+static cobalt_status check_dispatch(const int32_t* assigned, const int32_t* src, int64_t T,
+                                    int32_t K, int32_t G, const void* x, int64_t d,
+                                    const int32_t* counts, const int64_t* offsets,
+                                    const int32_t* pos, const void* packed) {
+    if (T < 0 || K < 1 || K > kMaxK || G < 1 || G > kMaxG) return COBALT_EINVAL;
+    if (!counts || !offsets) return COBALT_EINVAL;
+    if (T > 0 && (!assigned || !pos)) return COBALT_EINVAL;
+    if ((x == nullptr) != (packed == nullptr)) return COBALT_EINVAL;
+    if (x && (d < 8 || d % 8 != 0 || !aligned16(x) || !aligned16(packed))) return COBALT_EINVAL;
+    if (T * K >= (int64_t(1) << 31)) return COBALT_EUNSUPPORTED;
+    if (!src && T % G != 0) return COBALT_EINVAL;
+    return COBALT_OK;
+}
+
 extern "C" cobalt_status cobalt_dispatch_pack(const int32_t* assigned, const int32_t* src,
                                               int64_t T, int32_t K, int32_t G, const void* x,
                                               int64_t d, int32_t* counts, int64_t* offsets,
                                               int32_t* pos, void* packed, void* ws,
                                               size_t ws_bytes, void* stream) {
-    if (T < 0 || K < 1 || K > kMaxK || G < 1 || G > kMaxG) return COBALT_EINVAL;
-    if (!counts || !offsets || !ws) return COBALT_EINVAL;
-    if (T > 0 && (!assigned || !pos)) return COBALT_EINVAL;
-    if ((x == nullptr) != (packed == nullptr)) return COBALT_EINVAL;
-    if (x && (d < 8 || d % 8 != 0 || !aligned16(x) || !aligned16(packed))) return COBALT_EINVAL;
-    if (((uintptr_t)ws & 255u) != 0) return COBALT_EINVAL;
-    if (T * K >= (int64_t(1) << 31)) return COBALT_EUNSUPPORTED;
-    if (!src && T % G != 0) return COBALT_EINVAL;
+    if (cobalt_status st = check_dispatch(assigned, src, T, K, G, x, d, counts, offsets, pos,
+                                          packed))
+        return st;
+    if (!ws || ((uintptr_t)ws & 255u) != 0) return COBALT_EINVAL;
     if (ws_bytes < dispatch_workspace_bytes(T, K, G)) return COBALT_EINVAL;
+    return launch_dispatch(assigned, src, T, K, G, x, x ? d : 0, counts, offsets, pos, packed, ws,
+                           (hipStream_t)stream);
+}
+
+extern "C" cobalt_status cobalt_dispatch_pack_noalloc(const int32_t* assigned,
+                                                      const int32_t* src, int64_t T, int32_t K,
+                                                      int32_t G, const void* x, int64_t d,
+                                                      int32_t* counts, int64_t* offsets,
+                                                      int32_t* pos, void* packed, void* stream) {
+    if (cobalt_status st = check_dispatch(assigned, src, T, K, G, x, d, counts, offsets, pos,
+                                          packed))
+        return st;
+    if (dispatch_workspace_bytes(T, K, G) > COBALT_DISPATCH_NOALLOC_SCRATCH_BYTES)
+        return COBALT_EUNSUPPORTED;
+    void* ws = nullptr;
+    if (cobalt_status st = dispatch_noalloc_scratch(&ws)) return st;
     return launch_dispatch(assigned, src, T, K, G, x, x ? d : 0, counts, offsets, pos, packed, ws,
                            (hipStream_t)stream);
 }

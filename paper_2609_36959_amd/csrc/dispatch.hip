@@ -33,6 +33,8 @@
 // rows are written by node_scatter_kernel, four waves per (token, slice)
 // with two or four nodes each (copy_kernel for rows wider than 16 slices).
 #include <algorithm>
+#include <mutex>
+#include <vector>
 
 #include "internal.hpp"
 
@@ -772,6 +774,33 @@ cobalt_status launch_node_dispatch(const int32_t* assigned, const int32_t* src, 
         return COBALT_OK;
     }
     return launch_copy<true>(x, node_pos, T, N, d, bound, packed, s);
+}
+
+// Scratch of cobalt_dispatch_pack_noalloc: the dispatch workspace as a fixed
+// array in the library's device memory. Each GPU the library runs on holds
+// its own copy, from when the code object is loaded there until the process
+// ends. In host code the array's name denotes a host-side stand-in, not a
+// device address: the device address is looked up once per device and only
+// that address is handed to kernels. The init kernel clears the look-back
+// state and the tile counter at the start of every call, and the scan
+// writes every base entry before the rank kernel reads it, so what a
+// previous call left in the array does not matter.
+static __device__ __align__(256) uint8_t scratch[COBALT_DISPATCH_NOALLOC_SCRATCH_BYTES];
+
+cobalt_status dispatch_noalloc_scratch(void** out) {
+    static std::mutex mu;
+    static std::vector<void*> addr;  // per device
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return COBALT_EHIP;
+    std::lock_guard<std::mutex> lock(mu);
+    if ((int)addr.size() <= dev) addr.resize(dev + 1, nullptr);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return COBALT_EHIP;
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return COBALT_OK;
 }
 
 }  // namespace cobalt

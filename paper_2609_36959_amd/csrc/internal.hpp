@@ -77,6 +77,10 @@ cobalt_status launch_dispatch(const int32_t* assigned, const int32_t* src, int64
                               int G, const void* x, int64_t d, int32_t* counts,
                               int64_t* offsets, int32_t* pos, void* packed, void* ws,
                               hipStream_t s);
+// Device address of the fixed dispatch scratch on the current device
+// (COBALT_DISPATCH_NOALLOC_SCRATCH_BYTES bytes, 256-byte aligned); looked up
+// on the first call on each device, allocates nothing.
+cobalt_status dispatch_noalloc_scratch(void** out);
 size_t node_dispatch_workspace_bytes(int64_t T, int N, int G);
 cobalt_status launch_node_dispatch(const int32_t* assigned, const int32_t* src, int64_t T, int K,
                                    int N, int g, const void* x, int64_t d, int32_t* counts,

@@ -100,6 +100,21 @@ def test_argument_checks_reject_before_device_work():
                                   None) == EINVAL  # workspace too small
     assert L.cobalt_dispatch_pack(fake, None, 9, 2, 4, None, 0, fake, fake, fake, None, fake,
                                   1 << 20, None) == EINVAL  # T % G != 0 without src_rank
+    # workspace-free dispatch: the same checks, and sizes whose workspace
+    # exceeds the fixed scratch are refused before any device work
+    assert L.cobalt_dispatch_pack_noalloc(*args, fake, 8, fake, fake, fake, None,
+                                          None) == EINVAL
+    assert L.cobalt_dispatch_pack_noalloc(*args, fake, 12, fake, fake, fake, fake,
+                                          None) == EINVAL
+    assert L.cobalt_dispatch_pack_noalloc(fake, None, 9, 2, 4, None, 0, fake, fake, fake, None,
+                                          None) == EINVAL
+    cap = B.DISPATCH_NOALLOC_SCRATCH_BYTES
+    assert L.cobalt_dispatch_workspace_bytes(33486848, 1, 64) <= cap
+    assert L.cobalt_dispatch_workspace_bytes(33486848 + 2048, 1, 64) > cap
+    assert L.cobalt_dispatch_pack_noalloc(fake, None, 33486848 // 8 + 256, 8, 64, None, 0, fake,
+                                          fake, fake, None, None) == EUNSUPPORTED
+    assert L.cobalt_dispatch_pack_noalloc(fake, None, 900 * 512, 8, 512, None, 0, fake,
+                                          fake, fake, None, None) == EUNSUPPORTED
     # node dispatch: x without packed, null forwarding index, N or g out of
     # range, misaligned or short workspace, T % G != 0 without src_rank
     nargs = [fake, None, 8, 2, 2, 2]
