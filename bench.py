@@ -45,6 +45,11 @@ def parse():
     ap.add_argument("--cpu-sample-tokens", type=int, default=65536)
     ap.add_argument("--no-graph", action="store_true",
                     help="skip the extra timing of the step replayed as a HIP graph")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="time only the named workload (no per-workload summaries)")
+    ap.add_argument("--workloads", default="all",
+                    help="comma-separated workloads to summarise beside the named one "
+                         "(default: all five)")
     ap.add_argument("--replan", choices=("planner", "recipe"), default="planner",
                     help="multi-step workloads: re-plan the layout with the Stage-1 planner "
                          "from the EMA statistics, or with the workload's hot-order recipe")
@@ -105,34 +110,72 @@ def measured_traffic(call, workload):
         return None
 
 
-def routing_quality(st, torch, B, W):
+class RoutingTally:
     """Cross-node traffic (Eq. 1) of Algorithm 1 against two owner-only
-    baselines: on the same layout, and on plain contiguous expert parallelism
-    without replicas. Reporting only (outside the timed region)."""
-    w = st.w
+    baselines, summed over the steps added: owner-only on the same layout,
+    and owner-only on plain contiguous expert parallelism without replicas.
+    Sources are the contiguous blocks of the step. Reporting only (outside
+    the timed region)."""
 
-    def measure(layout, mode):
-        a = torch.empty_like(st.assigned)
-        rn = torch.empty_like(st.remote)
-        B.cobalt_assign(layout, st.topk, None, st.seed, 0, mode, a, rn)
+    def __init__(self, w, seed, torch, B, W):
+        self.w, self.seed, self.torch, self.B = w, seed, torch, B
+        t, o = W.contiguous_ep_layout(w)
+        self.ep = B.cobalt_layout_create(w.N, w.g, w.E, t.shape[1], t, o)
+        self.acc = {k: [0, 0, 0.0] for k in ("alg1", "owner_only", "contiguous_ep_owner_only")}
+        self.per_step_V = []
+        self.steps = 0
+
+    def _measure(self, layout, topk, step, mode):
+        torch, w = self.torch, self.w
+        a = torch.empty(w.T, w.K, dtype=torch.int32, device=topk.device)
+        rn = torch.empty(w.T, dtype=torch.int16, device=topk.device)
+        self.B.cobalt_assign(layout, topk, None, self.seed, step, mode, a, rn)
         torch.cuda.synchronize()
         src_node = (torch.arange(w.T, device=a.device) // (w.T // w.G)) // w.g
         cross = (a // w.g != src_node[:, None]).sum().item()
         rn32 = rn.to(torch.int32) & 0xFFFF
         V = sum(((rn32 >> n) & 1).sum().item() for n in range(w.N))
         load = torch.bincount(a.flatten(), minlength=w.G).float()
-        return {"V": int(V), "cross_pair_frac": cross / (w.T * w.K),
-                "imbalance": float(load.max() / load.mean())}
+        return int(V), int(cross), float(load.max() / load.mean())
 
-    out = {"alg1": measure(st.layout, 0), "owner_only": measure(st.layout, 1)}
-    t, o = W.contiguous_ep_layout(w)
-    L = B.cobalt_layout_create(w.N, w.g, w.E, t.shape[1], t, o)
-    out["contiguous_ep_owner_only"] = measure(L, 1)
-    B.cobalt_layout_destroy(L)
-    for k in ("owner_only", "contiguous_ep_owner_only"):
-        base = out[k]["V"]
-        out[f"V_reduction_vs_{k}"] = 1.0 - out["alg1"]["V"] / base if base else 0.0
-    return out
+    def add(self, layout, topk, step):
+        for key, L, mode in (("alg1", layout, 0), ("owner_only", layout, 1),
+                             ("contiguous_ep_owner_only", self.ep, 1)):
+            V, cross, imb = self._measure(L, topk, step, mode)
+            a = self.acc[key]
+            a[0] += V
+            a[1] += cross
+            a[2] += imb
+            if key == "alg1":
+                self.per_step_V.append(V)
+        self.steps += 1
+
+    def report(self):
+        w, n = self.w, max(self.steps, 1)
+        out = {k: {"V": a[0], "cross_pair_frac": a[1] / (n * w.T * w.K), "imbalance": a[2] / n}
+               for k, a in self.acc.items()}
+        for k in ("owner_only", "contiguous_ep_owner_only"):
+            base = out[k]["V"]
+            out[f"V_reduction_vs_{k}"] = 1.0 - out["alg1"]["V"] / base if base else 0.0
+        if self.steps > 1:
+            out["steps_summed"] = self.steps
+            out["alg1_V_per_step"] = self.per_step_V
+        return out
+
+    def close(self):
+        if self.ep is not None:
+            self.B.cobalt_layout_destroy(self.ep)
+            self.ep = None
+
+
+def routing_quality(st, torch, B, W):
+    """RoutingTally of the current step on the current layout."""
+    t = RoutingTally(st.w, st.seed, torch, B, W)
+    try:
+        t.add(st.layout, st.topk, 0)
+        return t.report()
+    finally:
+        t.close()
 
 
 def device_info(torch):
@@ -357,23 +400,12 @@ def cpu_baseline(st, n_tokens, torch, W, PL):
             "host_cpu": model, "host_cpus": os.cpu_count()}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has "
-              "no inter-GPU collectives; its virtual ranks are buffers on one GPU", file=sys.stderr)
-        sys.exit(2)
-    import torch
-
-    from paper_2609_36959_amd import binding as B
-    from paper_2609_36959_amd import pipeline as PL
-    from paper_2609_36959_amd import workload as W
-
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    B.lib()
-    w = W.WORKLOADS[args.workload]
-    seed = w.seed if args.seed is None else args.seed
+def run_workload(w, seed, steps, warmup, args, full, torch, B, PL, W):
+    """Times `steps` steps of workload w after `warmup` untimed ones and
+    returns the report. full=False keeps the timing, the roofline figures and
+    the routing quality; full=True adds the graph replay, the calls outside
+    the step, the HBM references, the node-deduplicated forms, the planner
+    demonstrations and the oracle's CPU baseline."""
     wl_name = f"t{w.T}_e{w.E}_k{w.K}_d{w.d}"
     st = PL.RoutingStep(w, seed=seed, device="cuda", expert_out="independent")
     stream = torch.cuda.Stream()
@@ -399,7 +431,7 @@ def main():
     del calib, calib_dst
 
     with torch.cuda.stream(stream):
-        for _ in range(args.warmup):
+        for _ in range(warmup):
             for f in fns:
                 f(stream=stream)
     torch.cuda.synchronize()
@@ -432,11 +464,11 @@ def main():
         st.coact.zero_()
         st.count.zero_()
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)]
-           for _ in range(args.steps)]
+           for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     with torch.cuda.stream(stream):
-        for k in range(args.steps):
+        for k in range(steps):
             if drift:
                 s = k % w.steps
                 if s == 0 and k > 0:
@@ -467,7 +499,7 @@ def main():
     call_ms = {c: 0.0 for c in calls}
     for e in evs:
         for i, c in enumerate(calls):
-            call_ms[c] += e[i].elapsed_time(e[i + 1]) / args.steps
+            call_ms[c] += e[i].elapsed_time(e[i + 1]) / steps
     ab = algorithmic_bytes(w)
     dominant = max(("cobalt_dispatch_pack", "cobalt_combine"), key=lambda c: call_ms[c])
     achieved = ab[dominant] / (call_ms[dominant] * 1e-3)
@@ -478,12 +510,12 @@ def main():
 
     result = {
         "metric": METRIC,
-        "value": w.T * args.steps / wall,
+        "value": w.T * steps / wall,
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": wall * 1e3 / args.steps,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": wall * 1e3 / steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -503,7 +535,7 @@ def main():
                      "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": achieved / HBM_PEAK,
                      "traffic": traffic},
         "pack_combine_hbm_frac": pc_bytes / pc_s / HBM_PEAK,
-        "step_hbm_frac": step_bytes / (wall / args.steps) / HBM_PEAK,
+        "step_hbm_frac": step_bytes / (wall / steps) / HBM_PEAK,
         "step_ms_percentiles": {"p10": pct(0.1), "median": pct(0.5), "p90": pct(0.9),
                                 "note": "per-step HIP events; value uses the wall clock"},
         "device": device_info(torch),
@@ -517,6 +549,7 @@ def main():
         st.coact.zero_()
         st.count.zero_()
         per_step = []
+        tally = RoutingTally(w, seed, torch, B, W)
         for s_ in range(w.steps):
             if s_ == w.swap_step:
                 torch.cuda.synchronize()
@@ -525,6 +558,7 @@ def main():
             st.step = s_
             for f in fns[:-2]:  # statistics, EMA and assignment
                 f()
+            tally.add(st.layout, st.topk, s_)
             rn32 = st.remote.to(torch.int32) & 0xFFFF
             V = sum(((rn32 >> n) & 1).sum().item() for n in range(w.N))
             per_rank = torch.bincount(st.assigned.flatten().long(), minlength=w.G).float()
@@ -532,7 +566,7 @@ def main():
         cycle_ms = [0.0] * w.steps
         for k, e in enumerate(evs):
             cycle_ms[k % w.steps] += e[0].elapsed_time(e[-1]) / sum(
-                1 for kk in range(args.steps) if kk % w.steps == k % w.steps)
+                1 for kk in range(steps) if kk % w.steps == k % w.steps)
         result["cycle_step_ms"] = [round(v, 4) for v in cycle_ms]
         before, after = per_step[:w.swap_step], per_step[w.swap_step:]
         result["replan"] = {"method": "stage1_planner" if planner else "hot_order_recipe",
@@ -545,6 +579,15 @@ def main():
             result["replan"].update({
                 "planner_host_ms": sum(p[0] for p in plan_info) / len(plan_info),
                 "objective": plan_info[-1][1], "plan_within_cap": plan_info[-1][2]})
+        result["routing"] = tally.report()
+        result["routing"]["note"] = ("summed over the cycle's steps, each on the layout it ran "
+                                     "on (re-planned before step %d)" % w.swap_step)
+        tally.close()
+    else:
+        result["routing"] = routing_quality(st, torch, B, W)
+    if not full:
+        st.close()
+        return result
 
     if not drift and not args.no_graph:
         # the same four calls captured once as a HIP graph and replayed
@@ -552,27 +595,27 @@ def main():
         torch.cuda.synchronize()
         with torch.cuda.graph(g):
             st.run()
-        for _ in range(args.warmup):
+        for _ in range(warmup):
             g.replay()
         torch.cuda.synchronize()
         tg = time.perf_counter()
-        for _ in range(args.steps):
+        for _ in range(steps):
             g.replay()
         torch.cuda.synchronize()
         wg = time.perf_counter() - tg
-        result["graph_replay"] = {"value": w.T * args.steps / wg, "unit": "tokens/s",
-                                  "ms_per_step": wg * 1e3 / args.steps}
+        result["graph_replay"] = {"value": w.T * steps / wg, "unit": "tokens/s",
+                                  "ms_per_step": wg * 1e3 / steps}
         del g
     # calls outside the step: per-replica load counts (the Stage-2 input)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     with torch.cuda.stream(stream):
         st.load(stream=stream)
         ev[0].record(stream)
-        for _ in range(args.steps):
+        for _ in range(steps):
             st.load(stream=stream)
         ev[1].record(stream)
     torch.cuda.synchronize()
-    result["extra_calls_ms"] = {"cobalt_replica_load": ev[0].elapsed_time(ev[1]) / args.steps}
+    result["extra_calls_ms"] = {"cobalt_replica_load": ev[0].elapsed_time(ev[1]) / steps}
     ref = hbm_reference(torch, stream)
     result["hbm_reference"] = ref
     result["call_frac_of_reference"] = {
@@ -585,11 +628,11 @@ def main():
     with torch.cuda.stream(stream):
         st.node_pack(stream=stream)
         ev[0].record(stream)
-        for _ in range(args.steps):
+        for _ in range(steps):
             st.node_pack(stream=stream)
         ev[1].record(stream)
     torch.cuda.synchronize()
-    node_ms = ev[0].elapsed_time(ev[1]) / args.steps
+    node_ms = ev[0].elapsed_time(ev[1]) / steps
     rows = int(st.node_offsets[-1].item())
     home = (torch.arange(w.T, device="cuda") // (w.T // w.G)) // w.g if st.src is None \
         else st.src.long() // w.g
@@ -607,11 +650,11 @@ def main():
     with torch.cuda.stream(stream):
         st.node_combine(stream=stream)
         ev[0].record(stream)
-        for _ in range(args.steps):
+        for _ in range(steps):
             st.node_combine(stream=stream)
         ev[1].record(stream)
     torch.cuda.synchronize()
-    ncb_ms = ev[0].elapsed_time(ev[1]) / args.steps
+    ncb_ms = ev[0].elapsed_time(ev[1]) / steps
     cb = node_combine_bytes(w, rows)
     result["extra_calls_ms"]["cobalt_node_combine"] = ncb_ms
     result["node_dedup_combine"] = {
@@ -629,11 +672,11 @@ def main():
     with torch.cuda.stream(stream):
         node_step()
         ev[0].record(stream)
-        for _ in range(args.steps):
+        for _ in range(steps):
             node_step()
         ev[1].record(stream)
     torch.cuda.synchronize()
-    nstep_ms = ev[0].elapsed_time(ev[1]) / args.steps
+    nstep_ms = ev[0].elapsed_time(ev[1]) / steps
     result["node_dedup_step"] = {"ms_per_step": nstep_ms, "value": w.T / (nstep_ms * 1e-3),
                                  "unit": "tokens/s",
                                  "calls": "stats + assign + node_dispatch_pack + node_combine"}
@@ -645,11 +688,11 @@ def main():
         st.stats(stream=stream)
         st.ema(0.9, B.EMA_INIT, stream=stream)
         ev[0].record(stream)
-        for _ in range(args.steps):
+        for _ in range(steps):
             st.ema(0.9, 0, stream=stream)
         ev[1].record(stream)
     torch.cuda.synchronize()
-    result["extra_calls_ms"]["cobalt_coact_ema"] = ev[0].elapsed_time(ev[1]) / args.steps
+    result["extra_calls_ms"]["cobalt_coact_ema"] = ev[0].elapsed_time(ev[1]) / steps
     pairs = torch.triu(st.coact != 0, diagonal=1)
     result["planner_statistics"] = {
         "ochiai_mean_coactivated_pairs": float(st.ochiai[pairs].mean().item()),
@@ -665,7 +708,6 @@ def main():
             float(st.ochiai[inside].mean().item())
         result["planner_statistics"]["ochiai_mean_other_pairs"] = \
             float(st.ochiai[pairs & same.logical_not()].mean().item())
-    result["routing"] = routing_quality(st, torch, B, W)
     result["routing"]["stage2_rebalance"] = stage2_demo(st, torch, B, W)
     result["routing"]["stage1_plan"] = stage1_demo(st, torch, B)
     if not args.no_cpu_baseline:
@@ -675,6 +717,67 @@ def main():
         result["replan"]["with_stage2_each_step"] = drift_with_stage2(
             st, w, routes, first_layout, replan, fns, torch, B)
     st.close()
+    return result
+
+
+ROUTING_KEYS = ("alg1", "owner_only", "contiguous_ep_owner_only", "V_reduction_vs_owner_only",
+                "V_reduction_vs_contiguous_ep_owner_only", "steps_summed", "alg1_V_per_step",
+                "note")
+
+
+def summarize(r):
+    """The per-workload entry of the report."""
+    out = {"config": r["config"]["workload"], "tokens_per_s": r["value"],
+           "ms_per_step": r["ms_per_step"], "steps": r["steps"], "warmup": r["warmup"],
+           "step_ms_median": r["step_ms_percentiles"]["median"],
+           "pack_combine_hbm_frac": r["pack_combine_hbm_frac"],
+           "step_hbm_frac": r["step_hbm_frac"], "call_ms": r["call_ms"],
+           "routing": {k: v for k, v in r["routing"].items() if k in ROUTING_KEYS}}
+    for k in ("cycle_step_ms", "replan"):
+        if k in r:
+            out[k] = r[k]
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has "
+              "no inter-GPU collectives; its virtual ranks are buffers on one GPU", file=sys.stderr)
+        sys.exit(2)
+    import gc
+
+    import torch
+
+    from paper_2609_36959_amd import binding as B
+    from paper_2609_36959_amd import pipeline as PL
+    from paper_2609_36959_amd import workload as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    B.lib()
+    w = W.WORKLOADS[args.workload]
+    seed = w.seed if args.seed is None else args.seed
+    print(f"bench: {w.name} ({w.describe()}), {args.steps} steps", file=sys.stderr, flush=True)
+    result = run_workload(w, seed, args.steps, args.warmup, args, True, torch, B, PL, W)
+    if not args.headline_only:
+        # every seeded workload once more, each at its default seed: the
+        # single-step ones over the same number of steps, the drift workload
+        # over one full cycle
+        wl = {}
+        names = W.NAMES if args.workloads == "all" else args.workloads.split(",")
+        for name in names:
+            if name == args.workload and args.seed is None:
+                wl[name] = summarize(result)
+                continue
+            gc.collect()
+            torch.cuda.empty_cache()
+            ow = W.WORKLOADS[name]
+            n = ow.steps if ow.steps > 1 else args.steps
+            print(f"bench: {name} ({ow.describe()}), {n} steps", file=sys.stderr, flush=True)
+            wl[name] = summarize(run_workload(ow, ow.seed, n, args.warmup, args, False, torch, B,
+                                              PL, W))
+        result["workloads"] = wl
     print(json.dumps(result), flush=True)
 
 

@@ -20,9 +20,10 @@ def test_more_than_one_gpu_is_refused():
 
 @pytest.mark.gpu
 def test_json_line_has_the_required_fields():
-    print("bench.py --workload tiny --steps 2 --warmup 1", flush=True)
+    print("bench.py --workload tiny --steps 2 --warmup 1 --workloads tiny,clusters-e64",
+          flush=True)
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "tiny",
-                        "--steps", "2", "--warmup", "1"],
+                        "--steps", "2", "--warmup", "1", "--workloads", "tiny,clusters-e64"],
                        capture_output=True, text=True, timeout=300, cwd=ROOT)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [ln for ln in r.stdout.splitlines() if ln.startswith("{")]
@@ -44,3 +45,14 @@ def test_json_line_has_the_required_fields():
     for key in ("value", "unit", "cores", "kind", "sample"):
         assert key in cpu, key
     assert cpu["kind"] == "oracle" and cpu["cores"] >= 1 and cpu["value"] > 0
+    # one summary per workload: throughput, HBM fractions, and Eq. 1's V for
+    # Algorithm 1 against both owner-only baselines
+    assert set(d["workloads"]) == {"tiny", "clusters-e64"}
+    for name, e in d["workloads"].items():
+        assert e["tokens_per_s"] > 0 and e["ms_per_step"] > 0, name
+        assert 0 < e["pack_combine_hbm_frac"] and 0 < e["step_hbm_frac"]
+        r_ = e["routing"]
+        for k in ("alg1", "owner_only", "contiguous_ep_owner_only"):
+            assert r_[k]["V"] >= 0 and 0 <= r_[k]["cross_pair_frac"] <= 1
+        # Algorithm 1 picks a minimum cover per token (Section 3.3)
+        assert r_["alg1"]["V"] <= r_["owner_only"]["V"]
