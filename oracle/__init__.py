@@ -71,11 +71,13 @@ def lib():
         L.ref_count_ema.argtypes = [P, i64, ctypes.c_float, i32, i32, P]
         L.ref_ochiai.argtypes = [P, P, i32, P]
         L.ref_plan_layout.argtypes = [i32, i32, i32, i32, P, P, ctypes.c_float, P, P, P, P, P]
+        L.ref_plan_exact.argtypes = [i32, i32, i32, i32, P, P, ctypes.c_float, P, P, P]
         L.ref_replica_load.argtypes = [P, P, i64, i32, i32, i32, P]
         L.ref_intra_node_rebalance.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P]
         for f in ("ref_coact_stats", "ref_layout_tables", "ref_assign", "ref_dispatch",
                   "ref_node_dispatch", "ref_combine", "ref_traffic", "ref_count_ema", "ref_ochiai",
-                  "ref_replica_load", "ref_intra_node_rebalance", "ref_plan_layout"):
+                  "ref_replica_load", "ref_intra_node_rebalance", "ref_plan_layout",
+                  "ref_plan_exact"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -327,3 +329,20 @@ def plan_layout(N, g, E, S, coact_ema, count_ema, eps):
     _check(lib().ref_plan_layout(N, g, E, S, _p(c), _p(w), float(eps), _p(table), _p(owner),
                                  _p(plan), ctypes.byref(obj), ctypes.byref(feas)), "plan_layout")
     return table, owner, plan, obj.value, bool(feas.value)
+
+
+def plan_exact(N, g, E, S, coact, work, eps):
+    """Eq. 3 solved exactly by enumeration (E <= 6, G <= 4). Returns
+    (found bool, objective float or None, slot_table [G, S] i32 or None)."""
+    G = N * g
+    c = _c(coact, np.float32)
+    w = _c(work, np.float32)
+    assert c.shape == (E, E) and w.shape == (E,)
+    table = np.zeros((G, S), np.int32)
+    found = ctypes.c_int32()
+    obj = ctypes.c_double()
+    _check(lib().ref_plan_exact(N, g, E, S, _p(c), _p(w), float(eps), ctypes.byref(found),
+                                ctypes.byref(obj), _p(table)), "plan_exact")
+    if not found.value:
+        return False, None, None
+    return True, obj.value, table

@@ -1425,3 +1425,123 @@ int ref_plan_layout(int32_t N, int32_t g, int32_t E, int32_t S, const float* coa
     if (feasible) *feasible = ok;
     return REF_OK;
 }
+
+/* ---------------------------------------------------------------------- */
+/* Stage 1 (Section 3.2, Eq. 3) solved exactly, for tiny instances only    */
+/* (E <= 6 experts, G <= 4 ranks). Every layout is visited: rank r takes a */
+/* set P_r of at most S experts (a bitmask over the experts), ranks in     */
+/* order and sets in increasing mask value. A layout counts if every       */
+/* expert has a replica and a division of the work exists; its value is    */
+/* Eq. 3's objective, the sum of c_ij over the pairs i < j whose experts   */
+/* both have a replica on a node, once for each such node. The first       */
+/* layout of the highest value is returned.                                */
+/*                                                                         */
+/* A division {w'_er} (w'_er >= 0, zero where e is not on r, sum_r w'_er = */
+/* w_e, sum_e w'_er <= cap on every rank) exists exactly when every set A  */
+/* of experts fits on the ranks that hold any of them:                     */
+/*     sum_{e in A} w_e <= cap * |{r : P_r meets A}|,                      */
+/* the supply-demand theorem for bipartite transport (Gale 1957), i.e.     */
+/* max-flow = min-cut on source -> e (capacity w_e) -> r (if e is on r,    */
+/* unbounded) -> sink (capacity cap). cap = (1 + eps) * sum_e w_e / G is   */
+/* the balance bound of Eq. 3 with the planned work in place of KT. A set  */
+/* fits when its work exceeds the bound by at most a relative 1e-9.        */
+/* Pair weights are read as given (only c_ij with i < j).                  */
+/* ---------------------------------------------------------------------- */
+struct exact_ctx {
+    int32_t N, g, E, S, G;
+    const float* c;
+    double w[6];
+    double cap;
+    uint32_t cur[4];   /* P_r of the layout being visited */
+    uint32_t best_layout[4];
+    double best;
+    int found;
+};
+
+static double exact_value(const struct exact_ctx* x)
+{
+    double v = 0.0;
+    for (int32_t n = 0; n < x->N; ++n) {
+        uint32_t on = 0; /* experts with a replica on node n */
+        for (int32_t i = 0; i < x->g; ++i) on |= x->cur[n * x->g + i];
+        for (int32_t a = 0; a < x->E; ++a)
+            for (int32_t b = a + 1; b < x->E; ++b)
+                if ((on >> a & 1u) && (on >> b & 1u)) v += (double)x->c[a * x->E + b];
+    }
+    return v;
+}
+
+static int exact_divisible(const struct exact_ctx* x)
+{
+    for (uint32_t A = 1; A < (1u << x->E); ++A) {
+        double need = 0.0;
+        int32_t holders = 0;
+        for (int32_t e = 0; e < x->E; ++e)
+            if (A >> e & 1u) need += x->w[e];
+        for (int32_t r = 0; r < x->G; ++r)
+            if (x->cur[r] & A) ++holders;
+        if (need > x->cap * (double)holders * (1.0 + 1e-9)) return 0;
+    }
+    return 1;
+}
+
+static void exact_visit(struct exact_ctx* x, int32_t r)
+{
+    if (r == x->G) {
+        uint32_t all = 0;
+        for (int32_t k = 0; k < x->G; ++k) all |= x->cur[k];
+        if (all != (1u << x->E) - 1u) return; /* an expert without a replica */
+        double v = exact_value(x);
+        if (x->found && !(v > x->best)) return; /* cannot replace the first best */
+        if (!exact_divisible(x)) return;
+        x->best = v;
+        memcpy(x->best_layout, x->cur, sizeof(x->cur));
+        x->found = 1;
+        return;
+    }
+    for (uint32_t m = 0; m < (1u << x->E); ++m) {
+        if (popcount32(m) > x->S) continue;
+        x->cur[r] = m;
+        exact_visit(x, r + 1);
+    }
+}
+
+/* Outputs: *found = 1 if some layout meets every constraint (else 0 and
+ * nothing else is written); *objective its value; slot_table [G][S] the
+ * first best layout, each rank's experts in increasing id, -1 after. */
+int ref_plan_exact(int32_t N, int32_t g, int32_t E, int32_t S, const float* coact,
+                   const float* work, float eps, int32_t* found, double* objective,
+                   int32_t* slot_table)
+{
+    if (N < 1 || g < 1 || N * g > 4 || E < 1 || E > 6 || S < 1 || !coact || !work || !found)
+        return REF_EINVAL;
+    if (!(eps >= 0.0f)) return REF_EINVAL;
+    struct exact_ctx x;
+    memset(&x, 0, sizeof(x));
+    x.N = N;
+    x.g = g;
+    x.E = E;
+    x.S = S;
+    x.G = N * g;
+    x.c = coact;
+    double total = 0.0;
+    for (int32_t e = 0; e < E; ++e) {
+        if (!(work[e] >= 0.0f) || isinf(work[e])) return REF_EINVAL;
+        x.w[e] = (double)work[e];
+        total += x.w[e];
+    }
+    x.cap = (1.0 + (double)eps) * total / (double)x.G;
+    exact_visit(&x, 0);
+    *found = x.found;
+    if (!x.found) return REF_OK;
+    if (objective) *objective = x.best;
+    if (slot_table) {
+        for (int32_t r = 0; r < x.G; ++r) {
+            int32_t k = 0;
+            for (int32_t e = 0; e < E; ++e)
+                if (x.best_layout[r] >> e & 1u) slot_table[r * S + k++] = e;
+            for (; k < S; ++k) slot_table[r * S + k] = -1;
+        }
+    }
+    return REF_OK;
+}

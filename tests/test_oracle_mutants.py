@@ -86,6 +86,18 @@ MUTANTS = [
     ("Stage 1 skips the repair across nodes",
      "for (int64_t moves = 0; moves < 4 * (int64_t)G * S; ++moves) {",
      "for (int64_t moves = 0; moves < 0; ++moves) {", ["test_oracle_plan.py"]),
+    ("exact Stage 1 counts a node's pairs on its first rank only",
+     "for (int32_t i = 0; i < x->g; ++i) on |= x->cur[n * x->g + i];",
+     "on = x->cur[n * x->g];", ["test_oracle_plan_exact.py"]),
+    ("exact Stage 1 ignores the work cap", "        if (!exact_divisible(x)) return;\n",
+     "", ["test_oracle_plan_exact.py"]),
+    ("exact Stage 1 needs every expert of a set on one rank",
+     "if (x->cur[r] & A) ++holders;", "if ((x->cur[r] & A) == A) ++holders;",
+     ["test_oracle_plan_exact.py"]),
+    ("exact Stage 1 allows one slot fewer", "if (popcount32(m) > x->S) continue;",
+     "if (popcount32(m) >= x->S) continue;", ["test_oracle_plan_exact.py"]),
+    ("exact Stage 1 keeps the last best layout", "if (x->found && !(v > x->best)) return;",
+     "if (x->found && !(v >= x->best)) return;", ["test_oracle_plan_exact.py"]),
     ("Stage 1 skips the retries with node slack",
      "for (int k = 0; k < 3 && !ok; ++k) {", "for (int k = 0; k < 0 && !ok; ++k) {",
      ["test_oracle_plan_milp.py"]),

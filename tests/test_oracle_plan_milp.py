@@ -13,9 +13,11 @@ from scipy.sparse import lil_matrix
 import oracle
 
 
-def eq3_milp(N, g, E, S, c, w, eps, time_limit):
+def eq3_milp(N, g, E, S, c, w, eps, time_limit, allow_infeasible=False):
     """x_er in {0,1}, u_en, z_ijn in [0,1], l_er >= 0 as in the appendix;
-    z only for pairs with c_ij > 0 (the others add nothing)."""
+    z only for pairs with c_ij > 0 (the others add nothing). Returns (best
+    objective, dual bound), or None for an infeasible instance when
+    allow_infeasible is set."""
     G = N * g
     pairs = [(i, j) for i in range(E) for j in range(i + 1, E) if c[i, j] > 0]
     nx, nu, nz = E * G, E * N, len(pairs) * N
@@ -64,6 +66,8 @@ def eq3_milp(N, g, E, S, c, w, eps, time_limit):
     ub[ol:] = np.inf
     res = milp(cost, constraints=LinearConstraint(A.tocsr(), lo, hi), integrality=integ,
                bounds=Bounds(np.zeros(nv), ub), options={"time_limit": time_limit})
+    if res.status == 2 and allow_infeasible:  # HiGHS: the problem is infeasible
+        return None
     assert res.x is not None, res.message
     return -res.fun, -res.mip_dual_bound
 
