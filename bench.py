@@ -189,19 +189,37 @@ def device_info(torch):
     return out
 
 
-def hbm_reference(torch, stream, reps=5):
-    """Measured HBM rates of plain torch kernels on 4 GiB buffers, on the
-    bench's stream: a fill (write only), a sum (read only) and a copy (read
-    and write). They show what a simple streaming kernel reaches on this
-    device, beside the 8 TB/s peak."""
+def hbm_reference(torch, stream, st, reps=5):
+    """HBM rates measured live on this device, on the bench's stream, with
+    the reference kernels of paper_2609_36959_amd/ceilings (each checked by
+    tests/test_gpu_ceilings.py to move the bytes it counts):
+    - read, write_fill, copy: one-pass streaming kernels on 4 GiB buffers
+      (16 B non-temporal accesses, one per thread), and torch's fill beside
+      them;
+    - pack_store: the pack's own store pattern on this step's pos (one
+      workgroup per token and 2 KiB slice, a 2 KiB burst per slot) without
+      its loads of x, the ceiling of the pack's write shape;
+    - gather_read: the combine's own loads of the K packed rows per token
+      and slice without the fold and the stores of y, the floor of its read
+      shape."""
+    from paper_2609_36959_amd import ceilings as CL
     n = 1 << 30  # int32 elements: 4 GiB
     a = torch.ones(n, dtype=torch.int32, device="cuda")
     b = torch.empty_like(a)
+    xo = torch.empty(CL.stream_blocks(4 * n), dtype=torch.int32, device="cuda")
+    w = st.w
+    groups = (w.d // 8 + 127) // 128
+    go = torch.empty(w.T * groups, dtype=torch.int32, device="cuda")
+    pk = w.T * w.K * w.d * 2
     out = {}
     with torch.cuda.stream(stream):
-        for name, fn, nbytes in (("write_fill", lambda: b.fill_(3), 4 * n),
-                                 ("read_sum", lambda: a.sum(), 4 * n),
-                                 ("copy", lambda: b.copy_(a), 8 * n)):
+        for name, fn, nbytes in (
+                ("read", lambda: CL.read(a, xo, stream=stream), 4 * n),
+                ("write_fill", lambda: CL.fill(b, stream=stream), 4 * n),
+                ("copy", lambda: CL.copy(a, b, stream=stream), 8 * n),
+                ("torch_fill", lambda: b.fill_(3), 4 * n),
+                ("pack_store", lambda: CL.pack_store(st.pos, st.packed, stream=stream), pk),
+                ("gather_read", lambda: CL.gather_read(st.eo, st.pos, go, stream=stream), pk)):
             fn()
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
             ev[0].record(stream)
@@ -209,10 +227,16 @@ def hbm_reference(torch, stream, reps=5):
                 fn()
             ev[1].record(stream)
             torch.cuda.synchronize()
-            out[name] = nbytes / (ev[0].elapsed_time(ev[1]) / reps * 1e-3) / 1e9
+            ms = ev[0].elapsed_time(ev[1]) / reps
+            out[name] = {"GB_s": round(nbytes / (ms * 1e-3) / 1e9, 1), "ms": round(ms, 4)}
     del a, b
     torch.cuda.empty_cache()
-    return {k: round(v, 1) for k, v in out.items()} | {"unit": "GB/s", "buffer": "4 GiB int32"}
+    # the pack's rows are rewritten by the step's own pack
+    with torch.cuda.stream(stream):
+        st.pack(stream=stream)
+    torch.cuda.synchronize()
+    return out | {"buffer": "4 GiB for the streaming kernels; this step's pos, packed rows and "
+                            "expert outputs for pack_store and gather_read"}
 
 
 def stage2_demo(st, torch, B, W):
@@ -616,12 +640,21 @@ def run_workload(w, seed, steps, warmup, args, full, torch, B, PL, W):
         ev[1].record(stream)
     torch.cuda.synchronize()
     result["extra_calls_ms"] = {"cobalt_replica_load": ev[0].elapsed_time(ev[1]) / steps}
-    ref = hbm_reference(torch, stream)
+    ref = hbm_reference(torch, stream, st)
     result["hbm_reference"] = ref
-    result["call_frac_of_reference"] = {
+    # the combine's floor: its row loads at the gather rate, then y at the fill rate
+    y_ms = w.T * w.d * 2 / (ref["write_fill"]["GB_s"] * 1e9) * 1e3
+    result["call_vs_ceiling"] = {
         "cobalt_dispatch_pack_vs_write_fill":
-            result["call_gbps"]["cobalt_dispatch_pack"] / ref["write_fill"],
-        "cobalt_combine_vs_copy": result["call_gbps"]["cobalt_combine"] / ref["copy"]}
+            result["call_gbps"]["cobalt_dispatch_pack"] / ref["write_fill"]["GB_s"],
+        "pack_store_ceiling_ms": ref["pack_store"]["ms"],
+        "cobalt_dispatch_pack_ms": call_ms["cobalt_dispatch_pack"],
+        "cobalt_dispatch_pack_time_vs_store_ceiling":
+            ref["pack_store"]["ms"] / call_ms["cobalt_dispatch_pack"],
+        "combine_floor_ms": ref["gather_read"]["ms"] + y_ms,
+        "cobalt_combine_ms": call_ms["cobalt_combine"],
+        "cobalt_combine_time_vs_floor": (ref["gather_read"]["ms"] + y_ms) / call_ms["cobalt_combine"],
+        "note": "time ratios: the ceiling's time over the call's (1.0 = at the ceiling)"}
     # the node-deduplicated dispatch of the last step's assignment: one row
     # per (token, destination node) instead of one per (token, expert)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]

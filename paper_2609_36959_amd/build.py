@@ -47,7 +47,25 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
+CEIL_SRC = os.path.join(PKG, "ceilings", "ceilings.hip")
+CEIL_LIB = os.path.join(PKG, "ceilings", "libceilings.so")
+
+
+def build_ceilings(verbose: bool = False) -> str:
+    """The benchmark's HBM reference kernels, a library of their own."""
+    tmp = CEIL_LIB + ".tmp"
+    cmd = [HIPCC, *HIPFLAGS, "-shared", CEIL_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {CEIL_SRC}:\n{r.stderr}")
+    os.replace(tmp, CEIL_LIB)
+    return CEIL_LIB
+
+
 def build(verbose: bool = False) -> str:
+    build_ceilings(verbose)
     os.makedirs(BUILD_DIR, exist_ok=True)
     srcs = sources()
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
