@@ -254,17 +254,28 @@ int ref_assign(int32_t N, int32_t g, int32_t E,
                 ++nU;
             }
         }
-        /* Start from all remote nodes, then scan every smaller candidate in
-         * increasing value and keep a feasible one with strictly fewer
-         * nodes: the first feasible minimum cover wins. */
+        /* b*: the fewest remote nodes that together hold every expert of
+         * U_t, a minimum cover of U_t by the nodes' expert sets; among the
+         * covers of that size, the one with the smallest remote mask (the
+         * order in which Algorithm 1 meets them). Node sets are tried by
+         * size, and within a size by mask value, and the first cover is
+         * kept. U_t empty is covered by no node at all. The set of all
+         * remote nodes always covers U_t on a valid layout (every expert
+         * has a replica, none of U_t's on the source node), so a cover is
+         * found; the all-remote mask stands in if the layout is invalid. */
         uint32_t full = (N > 1) ? ((1u << (N - 1)) - 1u) : 0u;
-        uint32_t bstar = full;
-        for (uint32_t b = 0; N > 1 && b + 1u <= full; ++b) {
-            int feasible = 1;
-            for (int32_t u = 0; u < nU; ++u)
-                if ((b & m[u]) == 0) { feasible = 0; break; }
-            if (feasible && popcount32(b) < popcount32(bstar)) bstar = b;
+        uint32_t bstar = 0;
+        int found = (nU == 0);
+        for (int32_t size = 1; !found && size <= N - 1; ++size) {
+            for (uint32_t b = 1; !found && b <= full; ++b) {
+                if (popcount32(b) != size) continue;
+                int covers = 1;
+                for (int32_t u = 0; u < nU; ++u)
+                    if ((b & m[u]) == 0) { covers = 0; break; }
+                if (covers) { bstar = b; found = 1; }
+            }
         }
+        if (!found) bstar = full;
         /* Each expert of U_t goes to a random node among the chosen ones
          * that hold it; the other experts stay on the source node. */
         for (int32_t j = 0; j < K; ++j) node_of[j] = home;

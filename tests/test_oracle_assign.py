@@ -187,7 +187,7 @@ def test_rank_choice_uniform_within_node():
     table = np.array([[0, 1], [0, -1], [0, -1], [-1, -1],
                       [1, -1], [-1, -1], [-1, -1], [-1, -1]], np.int32)
     tabs = oracle.layout_tables(N, g, E, table)
-    T = 30000
+    T = 300000  # 10^5 per candidate rank
     topk = np.zeros((T, 1), np.int32)
     src = np.full(T, 3, np.int32)
     a, _ = oracle.assign(N, g, E, tabs, topk, src, seed=11)
@@ -203,7 +203,7 @@ def test_node_choice_uniform_within_cover():
     N, g, E = 3, 1, 3
     table = np.array([[-1, -1], [0, 2], [1, 2]], np.int32)
     tabs = oracle.layout_tables(N, g, E, table)
-    T = 30000
+    T = 200000  # 10^5 per candidate node
     topk = np.tile(np.array([[0, 1, 2]], np.int32), (T, 1))
     src = np.zeros(T, np.int32)
     a, rn = oracle.assign(N, g, E, tabs, topk, src, seed=5, step=2)

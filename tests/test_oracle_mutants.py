@@ -25,8 +25,12 @@ MUTANTS = [
     ("bf16 ties round away from zero", "(lower == 0x8000u && (upper & 1u))",
      "(lower == 0x8000u)", ["test_oracle_bf16.py"]),
     ("Algorithm 1 keeps the last minimum cover",
-     "popcount32(b) < popcount32(bstar)) bstar = b;",
-     "popcount32(b) <= popcount32(bstar)) bstar = b;", ["test_oracle_assign.py"]),
+     "if (covers) { bstar = b; found = 1; }", "if (covers) { bstar = b; }",
+     ["test_oracle_assign.py"]),
+    ("Algorithm 1 skips covers of one node", "for (int32_t size = 1; !found",
+     "for (int32_t size = 2; !found", ["test_oracle_assign.py"]),
+    ("Algorithm 1 tries sets by value before size",
+     "                if (popcount32(b) != size) continue;\n", "", ["test_oracle_assign.py"]),
     ("remote mask keeps the home node's bit", "        if (n == home) continue;\n",
      "", ["test_oracle_assign.py"]),
     ("owner-only V counts the home node", "if (r / g != home) nodes |= 1u << (r / g);",

@@ -26,11 +26,12 @@ def test_pick_in_range_and_covers_all_values():
         assert ks == set(range(cnt))
 
 
-@pytest.mark.parametrize("cnt", [2, 3, 5, 7, 8, 31])
+@pytest.mark.parametrize("cnt", [2, 3, 5, 7, 8, 16, 31, 32])
 @pytest.mark.parametrize("stream", [0, 1])
 def test_pick_uniform_chi2(cnt, stream):
+    """10^5 draws for each candidate count, chi-square at the 1e-4 level."""
     key = oracle.rng_key(12345, 9)
-    n = 30000
+    n = 100000
     ks = np.array([oracle.pick(key, p, stream, cnt) for p in range(n)])
     _, pval = chisquare(np.bincount(ks, minlength=cnt))
     assert pval > 1e-4
@@ -39,7 +40,7 @@ def test_pick_uniform_chi2(cnt, stream):
 def test_streams_seeds_steps_decorrelated():
     """Node and rank draws of one pair, and draws of different steps or
     seeds, must not coincide systematically."""
-    n, cnt = 20000, 8
+    n, cnt = 100000, 8
     k1 = oracle.rng_key(1, 0)
     a = np.array([oracle.pick(k1, p, 0, cnt) for p in range(n)])
     b = np.array([oracle.pick(k1, p, 1, cnt) for p in range(n)])
@@ -47,7 +48,7 @@ def test_streams_seeds_steps_decorrelated():
     d = np.array([oracle.pick(oracle.rng_key(2, 0), p, 0, cnt) for p in range(n)])
     for other in (b, c, d):
         agree = np.mean(a == other)
-        assert abs(agree - 1 / cnt) < 0.02
+        assert abs(agree - 1 / cnt) < 0.01
         # joint distribution of (a, other) is uniform over cnt*cnt cells
         _, pval = chisquare(np.bincount(a * cnt + other, minlength=cnt * cnt))
         assert pval > 1e-4
