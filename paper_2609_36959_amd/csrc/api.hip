@@ -177,8 +177,8 @@ int64_t max_launch_items() {
 extern "C" size_t cobalt_coact_stats_workspace_bytes(int64_t T, int32_t K, int32_t E) {
     if (T < 0 || K < 1 || K > kMaxK || E < 1 || E > kMaxE) return 0;
     // the larger of the plans for 64 KiB and 160 KiB of LDS per workgroup
-    return std::max<size_t>(std::max<size_t>(coact_workspace_bytes(T, E, 64 * 1024),
-                                             coact_workspace_bytes(T, E, 160 * 1024)),
+    return std::max<size_t>(std::max<size_t>(coact_workspace_bytes(T, K, E, 64 * 1024),
+                                             coact_workspace_bytes(T, K, E, 160 * 1024)),
                             256);
 }
 

@@ -66,7 +66,7 @@ struct DeviceInfo {
 cobalt_status device_info(DeviceInfo* out);
 
 // Launchers (argument checks are done by the C entry points).
-size_t coact_workspace_bytes(int64_t T, int E, int lds_bytes);
+size_t coact_workspace_bytes(int64_t T, int K, int E, int lds_bytes);
 cobalt_status launch_coact_stats(const int32_t* topk, int64_t T, int K, int E, uint32_t* coact,
                                  uint32_t* count, void* ws, size_t ws_bytes, hipStream_t s);
 cobalt_status launch_assign(const DeviceLayout& L, const int32_t* topk, const int32_t* src,

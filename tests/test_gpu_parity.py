@@ -1,7 +1,7 @@
 """GPU parity: every step of the HIP path, called through the C ABI, against
 the oracle on the same seeded inputs, element by element. Sizes span
 several tiles with ragged tails; edge cases cover empty inputs, K = 1, one
-node, 16 nodes, tiny and long rows, and row bands of the statistics
+node, 16 nodes, tiny and long rows, and the row bands of the statistics
 histogram."""
 import numpy as np
 import pytest
@@ -166,9 +166,10 @@ def test_statistics_accumulate_across_calls():
 @pytest.mark.parametrize("E,T", [(384, 3000), (384, 70001), (1024, 3000), (4096, 2500),
                                  (2, 3000), (1, 100), (256, 131072 + 77)])
 def test_statistics_layouts(E, T):
-    """Pair histograms kept in LDS as 32-bit bins (E = 256), two 16-bit bins
-    per word (E = 384) and row bands (E = 1024, 4096), over one or many
-    token chunks with ragged tails."""
+    """Pair histograms in LDS as one band (E = 1, 2; small calls), in the
+    four interleaved row bands of large calls (E = 256, 384), and in as many
+    bands as the LDS needs (E = 384 at small T: 2, E = 1024: 16, E = 4096:
+    256), over one or many token chunks with ragged tails."""
     rng = np.random.default_rng(E + T)
     K = min(8, E)
     topk = np.argsort(rng.random((T, E)), axis=1)[:, :K].astype(np.int32)
