@@ -176,7 +176,7 @@ cobalt_status cobalt_dispatch_pack(const int32_t* assigned_rank, const int32_t* 
  * nothing; its first call on a device only looks up that device's copy.
  * Returns COBALT_EUNSUPPORTED, before anything is enqueued, when
  * cobalt_dispatch_workspace_bytes(T, K, G) exceeds the array (with G = 64
- * that is above 33 486 848 pairs T*K; with G = 512, above 3 667 968).
+ * that is above 66 973 696 pairs T*K; with G = 512, above 7 335 936).
  * Every call on one GPU uses that GPU's one array, and the array keeps what
  * the last call left in it (each call re-initialises what it reads), so
  * calls that may overlap on one GPU (different streams, or host threads

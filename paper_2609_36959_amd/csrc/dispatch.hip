@@ -46,16 +46,18 @@ constexpr int kCountThreads = 256;
 constexpr int kCountWin = 8192;  // LDS bins: (source - first source) * G + destination
 constexpr int kScanThreads = 1024;
 constexpr int kScanLds = 16384;  // G*G entries staged in LDS (G <= 128)
-constexpr int kRankWaves = 4;
-constexpr int kRankChunks = 8;
+constexpr int kRankWaves = 16;
+constexpr int kRankChunks = 4;
 constexpr int kRankThreads = kRankWaves * 64;
 constexpr int64_t kTile = (int64_t)kRankWaves * 64 * kRankChunks;  // pairs per tile
 constexpr uint64_t kFlagAgg = 1ull << 62;
 constexpr uint64_t kFlagInc = 2ull << 62;
 constexpr uint64_t kFlagMask = 3ull << 62;
 constexpr int kCopyWaves = 4;
+constexpr int kNodeWaves = 4;
+constexpr int kNodeThreads = kNodeWaves * 64;
 constexpr int kNodeChunks = 2;
-constexpr int64_t kNodeTile = (int64_t)kRankWaves * 64 * kNodeChunks;  // tokens per tile
+constexpr int64_t kNodeTile = (int64_t)kNodeWaves * 64 * kNodeChunks;  // tokens per tile
 
 struct Workspace {
     uint32_t* ctrl;    // [0] = next tile id
@@ -412,13 +414,13 @@ __global__ __launch_bounds__(kCountThreads) void node_count_kernel(
 //     base[s][n] + tile prefix + segment prefix + lanes below with bit n.
 // node_pos is written for every (t, n), -1 where the token has no row.
 template <int KC>
-__global__ __launch_bounds__(kRankThreads) void node_rank_kernel(
+__global__ __launch_bounds__(kNodeThreads) void node_rank_kernel(
     const int32_t* __restrict__ assigned, const int32_t* __restrict__ src, int64_t T, int Kr,
     int N, int g, int64_t tok_per_src, int64_t ntiles, uint32_t* __restrict__ ctrl,
     const int32_t* __restrict__ base, uint64_t* __restrict__ status,
     int32_t* __restrict__ node_pos, uint32_t* __restrict__ fwd, int32_t* __restrict__ row_token) {
     constexpr int KM = KC ? KC : kMaxK;
-    constexpr int kSegs = kRankWaves * kNodeChunks;
+    constexpr int kSegs = kNodeWaves * kNodeChunks;
     const int K = KC ? KC : Kr;
     const int G = N * g;
     __shared__ uint32_t seg[kSegs][kMaxN];  // segment counts, then segment prefixes
@@ -759,11 +761,11 @@ cobalt_status launch_node_dispatch(const int32_t* assigned, const int32_t* src, 
     if (cobalt_status st = launch_scan<true>(counts, G, N, offsets, w.base, s)) return st;
     if (T == 0) return COBALT_OK;
     if (K == 8)
-        hipLaunchKernelGGL(node_rank_kernel<8>, dim3((unsigned)w.ntiles), dim3(kRankThreads), 0,
+        hipLaunchKernelGGL(node_rank_kernel<8>, dim3((unsigned)w.ntiles), dim3(kNodeThreads), 0,
                            s, assigned, src, T, K, N, g, tok_per_src, w.ntiles, w.ctrl, w.base,
                            w.status, node_pos, fwd, row_token);
     else
-        hipLaunchKernelGGL(node_rank_kernel<0>, dim3((unsigned)w.ntiles), dim3(kRankThreads), 0,
+        hipLaunchKernelGGL(node_rank_kernel<0>, dim3((unsigned)w.ntiles), dim3(kNodeThreads), 0,
                            s, assigned, src, T, K, N, g, tok_per_src, w.ntiles, w.ctrl, w.base,
                            w.status, node_pos, fwd, row_token);
     COBALT_LAUNCH_CHECK();

@@ -109,11 +109,11 @@ def test_argument_checks_reject_before_device_work():
     assert L.cobalt_dispatch_pack_noalloc(fake, None, 9, 2, 4, None, 0, fake, fake, fake, None,
                                           None) == EINVAL
     cap = B.DISPATCH_NOALLOC_SCRATCH_BYTES
-    assert L.cobalt_dispatch_workspace_bytes(33486848, 1, 64) <= cap
-    assert L.cobalt_dispatch_workspace_bytes(33486848 + 2048, 1, 64) > cap
-    assert L.cobalt_dispatch_pack_noalloc(fake, None, 33486848 // 8 + 256, 8, 64, None, 0, fake,
+    assert L.cobalt_dispatch_workspace_bytes(66973696, 1, 64) <= cap
+    assert L.cobalt_dispatch_workspace_bytes(66973696 + 4096, 1, 64) > cap
+    assert L.cobalt_dispatch_pack_noalloc(fake, None, 66973696 // 8 + 256, 8, 64, None, 0, fake,
                                           fake, fake, None, None) == EUNSUPPORTED
-    assert L.cobalt_dispatch_pack_noalloc(fake, None, 900 * 512, 8, 512, None, 0, fake,
+    assert L.cobalt_dispatch_pack_noalloc(fake, None, 1800 * 512, 8, 512, None, 0, fake,
                                           fake, fake, None, None) == EUNSUPPORTED
     # node dispatch: x without packed, null forwarding index, N or g out of
     # range, misaligned or short workspace, T % G != 0 without src_rank

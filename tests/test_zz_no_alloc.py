@@ -92,9 +92,9 @@ def test_noalloc_matches_workspace_dispatch_on_shrinking_calls():
 
 
 def test_noalloc_layout_only_near_the_scratch_limit():
-    # G = 64: the scratch holds the look-back state of up to 33 486 848 pairs
-    G, K = 64, 8
-    T = 33486848 // K // G * G
+    # G = 512: the scratch holds the look-back state of up to 7 335 936 pairs
+    G, K = 512, 8
+    T = 7335936 // K // G * G
     assert B.cobalt_dispatch_workspace_bytes(T, K, G) <= B.DISPATCH_NOALLOC_SCRATCH_BYTES
     print(f"noalloc layout-only call: T={T} K={K} G={G}", flush=True)
     a, src, _ = _inputs(T, K, G, 0, "null", seed=7)
@@ -106,7 +106,7 @@ def test_noalloc_layout_only_near_the_scratch_limit():
 
 def test_noalloc_rejects_sizes_beyond_the_scratch():
     G, K = 64, 8
-    T = (33486848 // K // G + 64) * G
+    T = (66973696 // K // G + 64) * G
     assert B.cobalt_dispatch_workspace_bytes(T, K, G) > B.DISPATCH_NOALLOC_SCRATCH_BYTES
     a = torch.zeros(T, K, dtype=torch.int32, device="cuda")
     counts = torch.zeros(G, G, dtype=torch.int32, device="cuda")
