@@ -548,9 +548,13 @@ __global__ __launch_bounds__(kMaxK * 64) void scatter_kernel(
     if (in1) v1 = row[c0 + 64];
     const int p = pos[(int64_t)t * K + j];
     if (p < 0 || p >= bound) return;
+    // The row's buffer descriptor drops stores past its nch chunks, so the
+    // stores need no guard of their own: both issue back to back from one
+    // offset register.
     u32x4* dst = packed + (int64_t)p * nch;
-    if (in0) __builtin_nontemporal_store(v0, dst + c0);
-    if (in1) __builtin_nontemporal_store(v1, dst + c0 + 64);
+    const int32_t off = (int32_t)(c0 * 16);
+    store_stream(v0, dst, (int32_t)(nch * 16), off);
+    store_stream(v1, dst, (int32_t)(nch * 16), off + 1024);
 }
 
 // Launches scatter_kernel for rows pos[t][0..per_tok) in [0, bound) when

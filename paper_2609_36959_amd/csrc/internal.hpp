@@ -19,6 +19,21 @@ constexpr int kMaxE = 4096;
 
 // 16-byte vector: eight bf16 values, the unit of every row copy.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Streaming row store: a 16-byte raw buffer store with the non-temporal
+// (nt) cache bit, through a buffer descriptor of `bytes` bytes at `base`.
+// The hardware drops stores outside the descriptor, so a row's stores need
+// no guard branches of their own and issue back to back from one offset
+// register (with a branch per store the compiler can make the second wait
+// for the first). The descriptor's third dword is the gfx9 raw-buffer
+// format word.
+__device__ __forceinline__ void store_stream(const u32x4& v, void* base, int32_t bytes,
+                                             int32_t offset) {
+    constexpr int kNt = 2;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(base, (short)0, bytes, 0x00020000);
+    __builtin_amdgcn_raw_buffer_store_b128(v, rs, offset, 0, kNt);
+}
 // 8-byte vector: four bf16 values.
 
 struct DeviceLayout {
