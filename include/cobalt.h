@@ -91,16 +91,19 @@ cobalt_status cobalt_layout_tables(cobalt_layout_t layout, uint32_t* host_node_m
  * expert_count[topk_idx[t][a]] += 1. Nothing is zeroed: counts accumulate
  * across calls (and steps) until the caller clears them. With distinct
  * experts per token coact is symmetric with a zero diagonal and row sums
- * (K-1) * expert_count.
+ * (K-1) * expert_count; an expert a token holds m times adds m(m-1) to
+ * its diagonal entry. Ids outside [0, E) count nowhere.
  * K > E is rejected with COBALT_EINVAL (a token's experts are distinct).
  * workspace: device scratch of at least cobalt_coact_stats_workspace_bytes(
- *   T, K, E) bytes (partial histograms, about 4 * min(64, T/2048) * E(E-1)/2
- *   bytes), 256-byte aligned, owned by the caller; contents on entry are
- *   ignored; it must not be shared by calls that may overlap. The call
- *   updates coact and expert_count with plain (non-atomic) adds, or with
- *   integer atomic adds when it is small (at most 65536 bin updates), so
- *   calls that may overlap must not share them either. The counts are exact
- *   either way and do not depend on scheduling.
+ *   T, K, E) bytes (partial histograms of E(E-1)/2 bins for each chunk of
+ *   about 1024 tokens, at most 128 chunks; 2 bytes per bin where a chunk's
+ *   bins cannot pass 65535, else 4), 256-byte aligned, owned by the
+ *   caller; contents on entry are ignored; it must not be shared by calls
+ *   that may overlap. The call updates coact and expert_count with plain
+ *   (non-atomic) adds, or with integer atomic adds when it is small (at most
+ *   65536 bin updates) and on the diagonal, so calls that may overlap must
+ *   not share them either. The counts are exact either way and do not
+ *   depend on scheduling.
  * ---------------------------------------------------------------------- */
 size_t cobalt_coact_stats_workspace_bytes(int64_t T, int32_t K, int32_t E);
 

@@ -181,6 +181,72 @@ def test_statistics_layouts(E, T):
     assert np.array_equal(u32(count), cnt)
 
 
+def _stats_check(topk, E):
+    T, K = topk.shape
+    coact = torch.zeros(E, E, dtype=torch.int32, device="cuda")
+    count = torch.zeros(E, dtype=torch.int32, device="cuda")
+    B.cobalt_coact_stats(dev_i32(topk), E, coact, count, B.stats_workspace_for(T, K, E))
+    C, cnt = oracle.coact_stats(topk, E)
+    assert np.array_equal(u32(coact), C)
+    assert np.array_equal(u32(count), cnt)
+
+
+def test_statistics_uint32_partials():
+    """K = 16 over 140 000 tokens: 128 chunks of 1094 tokens could pass
+    65535 in a bin (64 per token at most), so the partials are uint32."""
+    rng = np.random.default_rng(11)
+    T, E, K = 140000, 64, 16
+    _stats_check(np.argsort(rng.random((T, E)), axis=1)[:, :K].astype(np.int32), E)
+
+
+def test_statistics_uint16_bound():
+    """128 chunks of 4095 tokens that each add 16 to the pair (3, 5) (ids 3
+    and 5 four times each): every chunk's bin holds 65520, the most a uint16
+    partial is trusted with."""
+    T = 4095 * 128
+    topk = np.tile(np.array([3, 3, 3, 3, 5, 5, 5, 5], np.int32), (T, 1))
+    _stats_check(topk, 16)
+
+
+def _stats_valid_slots(topk, E):
+    """The statistics with ids outside [0, E) dropped: every ordered pair of
+    distinct slots whose ids are both in range, and every such slot."""
+    T, K = topk.shape
+    C = np.zeros((E, E), np.uint64)
+    cnt = np.zeros(E, np.uint64)
+    ok = (topk >= 0) & (topk < E)
+    for a in range(K):
+        np.add.at(cnt, topk[ok[:, a], a], 1)
+        for b in range(K):
+            if a != b:
+                m = ok[:, a] & ok[:, b]
+                np.add.at(C, (topk[m, a], topk[m, b]), 1)
+    return C.astype(np.uint32), cnt.astype(np.uint32)
+
+
+def test_statistics_mixed_waves():
+    """Tokens with repeated ids (m copies add m(m - 1) to the diagonal) or
+    out-of-range ids (which count nowhere) scattered among valid ones, so
+    that some waves take the per-pair checks and the rest skip them."""
+    rng = np.random.default_rng(12)
+    T, E, K = 3 * 2048 + 5, 40, 8
+    topk = np.argsort(rng.random((T, E)), axis=1)[:, :K].astype(np.int32)
+    rows = rng.choice(T, size=60, replace=False)
+    topk[rows[:20], 3] = topk[rows[:20], 6]            # an id twice
+    topk[rows[20:30], 1:4] = topk[rows[20:30], :1]     # an id four times
+    topk[rows[30:], 0] = rng.choice([-1, E, -7], size=30)  # out of range
+    # the brute force agrees with the oracle where every id is in range
+    good = np.setdiff1d(np.arange(T), rows[30:])
+    assert all(np.array_equal(x, y) for x, y in
+               zip(_stats_valid_slots(topk[good], E), oracle.coact_stats(topk[good], E)))
+    C, cnt = _stats_valid_slots(topk, E)
+    coact = torch.zeros(E, E, dtype=torch.int32, device="cuda")
+    count = torch.zeros(E, dtype=torch.int32, device="cuda")
+    B.cobalt_coact_stats(dev_i32(topk), E, coact, count, B.stats_workspace_for(T, K, E))
+    assert np.array_equal(u32(coact), C)
+    assert np.array_equal(u32(count), cnt)
+
+
 def _custom(N, g, E, S, K, T, d, seed, extra_per_rank=None):
     w = W.Workload("custom", T, E, K, d, N, g, S)
     rng = np.random.default_rng(seed)
