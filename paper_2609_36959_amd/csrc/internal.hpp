@@ -34,7 +34,6 @@ __device__ __forceinline__ void store_stream(const u32x4& v, void* base, int32_t
         __builtin_amdgcn_make_buffer_rsrc(base, (short)0, bytes, 0x00020000);
     __builtin_amdgcn_raw_buffer_store_b128(v, rs, offset, 0, kNt);
 }
-// 8-byte vector: four bf16 values.
 
 struct DeviceLayout {
     int device;
