@@ -19,13 +19,14 @@
 //           e[b]) of the later slots, with LDS atomics. The band's bins are
 //           then written to the chunk's slot of the workspace, as uint16
 //           where no bin of a chunk can pass 65535, else as uint32.
-//   reduce  eight lanes per group of eight band bins sum the group over the
-//           chunks (lane k takes chunks k, k + 8, ..., one 16-byte load of
-//           eight uint16 bins each), then exchange halves in three shuffle
-//           rounds so that lane k ends with the total of bin k, which it
-//           adds to coact[i][j] and coact[j][i]. Other lanes do the same for
-//           expert_count. Every output element has exactly one writer, so
-//           the result does not depend on scheduling.
+//   reduce  sixteen lanes per group of eight band bins sum the group over
+//           the chunks (lane k takes chunks k, k + 16, ..., one 16-byte load
+//           of eight uint16 bins each), add pairwise across lanes k and
+//           k + 8, then exchange halves in three shuffle rounds so that lane
+//           k < 8 ends with the total of bin k, which it adds to coact[i][j]
+//           and coact[j][i]. Other lanes do the same for expert_count. Every
+//           output element has exactly one writer, so the result does not
+//           depend on scheduling.
 //
 // Checks. Ids outside [0, E) count nowhere. A token that repeats an id adds
 // the product of the multiplicities to a pair, and m (m - 1) to the
@@ -55,7 +56,7 @@ namespace {
 
 constexpr int kCountThreads = 1024;
 constexpr int kReduceThreads = 256;
-constexpr int kReduceLanes = 8;  // lanes per group of eight bins (and per count)
+constexpr int kReduceLanes = 16;  // lanes per group of eight bins (and per count)
 constexpr int kMaxLgBands = 12;
 constexpr int64_t kTokensPerChunk = 1024;
 constexpr int64_t kMaxChunks = 128;
@@ -339,7 +340,8 @@ __global__ __launch_bounds__(kReduceThreads) void coact_reduce_kernel(
     const void* __restrict__ part, const uint32_t* __restrict__ cpart, int E, int lgb,
     int nchunks, int64_t band_stride, bool do_count, uint32_t* __restrict__ coact,
     uint32_t* __restrict__ count) {
-    static_assert(kReduceLanes == 8, "one lane per bin of a group of eight");
+    static_assert(kReduceLanes >= 8 && kReduceLanes <= 64 && (kReduceLanes & (kReduceLanes - 1)) == 0,
+                  "a power of two of at least eight lanes");
     const int nb = 1 << lgb;
     const int64_t groups_per_band = band_stride / 8;
     const int64_t ngroups = (int64_t)nb * groups_per_band;
@@ -349,10 +351,11 @@ __global__ __launch_bounds__(kReduceThreads) void coact_reduce_kernel(
     if (item < ngroups) {
         const int band = (int)(item / groups_per_band);
         const int32_t w0 = (int32_t)(item % groups_per_band) * 8;
-        // Lane k's bin and its two outputs, read before the partials so that
-        // both loads are in flight together.
-        const int32_t w = w0 + k;
-        const bool real = w < band_words(E, nb, band);
+        // The bin of lane k < 8 and its two outputs, read before the
+        // partials so that both loads are in flight together; lanes from 8 on
+        // help with the sums only.
+        const int32_t w = w0 + (k & 7);
+        const bool real = k < 8 && w < band_words(E, nb, band);
         int64_t ij = 0, ji = 0;
         uint32_t cij = 0, cji = 0;
         if (real) {
@@ -390,9 +393,14 @@ __global__ __launch_bounds__(kReduceThreads) void coact_reduce_kernel(
                 }
             }
         }
-        // Three rounds, each halving the bins a lane holds: the lane keeps
-        // the half its bit selects and adds the partner's sums of that half.
-        // Lane k ends with the total of bin w0 + k.
+        // Lanes k, k ^ 8, k ^ 16, ... add their sums, then three rounds each
+        // halve the bins a lane holds: the lane keeps the half its bit
+        // selects and adds the partner's sums of that half. Lane k ends with
+        // the total of bin w0 + k % 8.
+#pragma unroll
+        for (int o = 8; o < kReduceLanes; o <<= 1)
+#pragma unroll
+            for (int m = 0; m < 8; ++m) s[m] += __shfl_xor(s[m], o, kReduceLanes);
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             const bool up = k & 4;
