@@ -31,10 +31,18 @@ constexpr int kCombineWaves = 16;
 constexpr int kFoldWaves = 2;  // waves that fold or sum a staged slice (128 chunks, one per thread)
 constexpr int kNodeWaves = 4;  // least waves of node_fold_kernel; waves of node_sum_kernel
 
-__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (u >> 16) | 0x40u;
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Rounds a and b to bf16, nearest even, and packs them with a in the low
+// half: one v_cvt_pk_bf16_f32. In the floating-point mode of these kernels
+// (IEEE, fp32 denormals kept) it gives the bits of the IEEE-754 rule written
+// out (a quiet NaN keeps its sign and the top bits of its payload) on every
+// one of the 2^32 inputs, and costs one instruction where the bit rule
+// costs about ten for the pair.
+__device__ __forceinline__ uint32_t pack_bf16_rne(float a, float b) {
+    const f32x2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
 // KC = compile-time K (0: any K up to 16, read at run time); with KC the
@@ -88,7 +96,7 @@ __global__ __launch_bounds__(kCombineWaves * 64) void combine_kernel(
     u32x4 out;
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-        out[q] = f32_to_bf16_rne(acc[2 * q]) | (f32_to_bf16_rne(acc[2 * q + 1]) << 16);
+        out[q] = pack_bf16_rne(acc[2 * q], acc[2 * q + 1]);
     __builtin_nontemporal_store(out, y + t * nch + c);
     if (kF32) {
         float4* o = (float4*)(y32 + (t * nch + c) * 8);
@@ -154,7 +162,7 @@ __global__ __launch_bounds__(kMaxK * 64) void fold_kernel(
     u32x4 out;
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-        out[q] = f32_to_bf16_rne(acc[2 * q]) | (f32_to_bf16_rne(acc[2 * q + 1]) << 16);
+        out[q] = pack_bf16_rne(acc[2 * q], acc[2 * q + 1]);
     __builtin_nontemporal_store(out, y + (int64_t)t * nch + c);
     if (kF32) {
         float4* o = (float4*)(y32 + ((int64_t)t * nch + c) * 8);
@@ -261,7 +269,7 @@ __global__ __launch_bounds__(kMaxK * 64) void node_fold_kernel(
             u32x4 out;
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                out[e] = f32_to_bf16_rne(acc[h][2 * e]) | (f32_to_bf16_rne(acc[h][2 * e + 1]) << 16);
+                out[e] = pack_bf16_rne(acc[h][2 * e], acc[h][2 * e + 1]);
             __builtin_nontemporal_store(out, dst + c0 + 64 * h);
         }
     }
@@ -357,7 +365,7 @@ __global__ __launch_bounds__(kNodeWaves * 64) void node_sum_kernel(
     u32x4 out;
 #pragma unroll
     for (int h = 0; h < 4; ++h)
-        out[h] = f32_to_bf16_rne(acc[2 * h]) | (f32_to_bf16_rne(acc[2 * h + 1]) << 16);
+        out[h] = pack_bf16_rne(acc[2 * h], acc[2 * h + 1]);
     __builtin_nontemporal_store(out, y + (int64_t)t * nch + c);
 }
 
