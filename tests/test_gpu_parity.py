@@ -224,12 +224,14 @@ def _stats_valid_slots(topk, E):
     return C.astype(np.uint32), cnt.astype(np.uint32)
 
 
-def test_statistics_mixed_waves():
+@pytest.mark.parametrize("T,E", [(3 * 2048 + 5, 40), (131072 + 5, 256)])
+def test_statistics_mixed_waves(T, E):
     """Tokens with repeated ids (m copies add m(m - 1) to the diagonal) or
     out-of-range ids (which count nowhere) scattered among valid ones, so
-    that some waves take the per-pair checks and the rest skip them."""
+    that some waves take the per-pair checks and the rest skip them; the
+    second size runs the two-band plan with uint16 partials."""
     rng = np.random.default_rng(12)
-    T, E, K = 3 * 2048 + 5, 40, 8
+    K = 8
     topk = np.argsort(rng.random((T, E)), axis=1)[:, :K].astype(np.int32)
     rows = rng.choice(T, size=60, replace=False)
     topk[rows[:20], 3] = topk[rows[:20], 6]            # an id twice
