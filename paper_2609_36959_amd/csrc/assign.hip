@@ -64,16 +64,36 @@ struct Swar {
     __device__ static bool has_zero_lane(uint64_t v) { return ((v - kOnes) & ~v & kHigh) != 0; }
 };
 
-template <int LB>
+// Writes a token's K ranks: two 16-byte stores for K = 8 (KV), one 4-byte
+// store per slot otherwise.
+template <bool KV>
+__device__ __forceinline__ void store_ranks(int32_t* out, int K, const int (&r)[kMaxK]) {
+    if constexpr (KV) {
+        int4* o = reinterpret_cast<int4*>(out);
+        o[0] = make_int4(r[0], r[1], r[2], r[3]);
+        o[1] = make_int4(r[4], r[5], r[6], r[7]);
+    } else {
+#pragma unroll
+        for (int j = 0; j < kMaxK; ++j)
+            if (j < K) out[j] = r[j];
+    }
+}
+
+// KV: K = 8 with 16-byte aligned topk and out, read and written with two
+// 16-byte accesses per token.
+template <int LB, bool KV>
 __global__ __launch_bounds__(kAssignThreads) void assign_kernel(AssignArgs a) {
     using SW = Swar<LB>;
     const int64_t t = (int64_t)blockIdx.x * kAssignThreads + threadIdx.x;
     if (t >= a.T) return;
-    const int K = a.K;
+    const int K = KV ? 8 : a.K;
     const int64_t p0 = t * K;
     const int s = a.src ? a.src[t] : (int)(t / a.tok_per_src);
+    int rr[kMaxK];
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) rr[j] = -1;
     if (s < 0 || s >= a.G) {
-        for (int j = 0; j < K; ++j) a.out[p0 + j] = -1;
+        store_ranks<KV>(a.out + p0, K, rr);
         if (a.remote) a.remote[t] = 0;
         return;
     }
@@ -82,29 +102,30 @@ __global__ __launch_bounds__(kAssignThreads) void assign_kernel(AssignArgs a) {
     const uint32_t low = home_bit - 1u;
 
     int e[kMaxK];
+    if constexpr (KV) {
+        const int4* q = reinterpret_cast<const int4*>(a.topk + p0);
+        const int4 v0 = q[0], v1 = q[1];
+        e[0] = v0.x; e[1] = v0.y; e[2] = v0.z; e[3] = v0.w;
+        e[4] = v1.x; e[5] = v1.y; e[6] = v1.z; e[7] = v1.w;
+    }
 #pragma unroll
     for (int j = 0; j < kMaxK; ++j) {
-        e[j] = -1;
-        if (j < K) {
-            const int v = a.topk[p0 + j];
-            e[j] = (v >= 0 && v < a.E) ? v : -1;
-        }
+        if constexpr (!KV) e[j] = j < K ? a.topk[p0 + j] : -1;
+        if (j >= K) e[j] = -1;
+        e[j] = (e[j] >= 0 && e[j] < a.E) ? e[j] : -1;
     }
 
     if (a.mode == 1) {  // owner-only baseline
         uint32_t nodes = 0;
 #pragma unroll
         for (int j = 0; j < kMaxK; ++j) {
-            if (j < K) {
-                int r = -1;
-                if (e[j] >= 0) {
-                    r = a.owner[e[j]];
-                    const int n = r / a.g;
-                    if (n != home) nodes |= 1u << n;
-                }
-                a.out[p0 + j] = r;
+            if (j < K && e[j] >= 0) {
+                rr[j] = a.owner[e[j]];
+                const int n = rr[j] / a.g;
+                if (n != home) nodes |= 1u << n;
             }
         }
+        store_ranks<KV>(a.out + p0, K, rr);
         if (a.remote) a.remote[t] = (uint16_t)nodes;
         return;
     }
@@ -178,23 +199,20 @@ __global__ __launch_bounds__(kAssignThreads) void assign_kernel(AssignArgs a) {
     // Node of each task, then its rank (Step 2).
 #pragma unroll
     for (int j = 0; j < kMaxK; ++j) {
-        if (j < K) {
+        if (j < K && e[j] >= 0) {
             const int64_t p = p0 + j;
-            int r = -1;
-            if (e[j] >= 0) {
-                int n = home;
-                const uint32_t cand = bstar & m[j];  // empty only on invalid layouts
-                if (m[j] && cand) {
-                    const int bit = kth_bit(cand, draw(a.key, p, 0, __builtin_popcount(cand)));
-                    n = bit + (bit >= home ? 1 : 0);
-                }
-                const uint32_t R = a.rank_mask[(int64_t)e[j] * a.N + n];
-                if ((!m[j] || cand) && R)
-                    r = n * a.g + kth_bit(R, draw(a.key, p, 1, __builtin_popcount(R)));
+            int n = home;
+            const uint32_t cand = bstar & m[j];  // empty only on invalid layouts
+            if (m[j] && cand) {
+                const int bit = kth_bit(cand, draw(a.key, p, 0, __builtin_popcount(cand)));
+                n = bit + (bit >= home ? 1 : 0);
             }
-            a.out[p] = r;
+            const uint32_t R = a.rank_mask[(int64_t)e[j] * a.N + n];
+            if ((!m[j] || cand) && R)
+                rr[j] = n * a.g + kth_bit(R, draw(a.key, p, 1, __builtin_popcount(R)));
         }
     }
+    store_ranks<KV>(a.out + p0, K, rr);
     if (a.remote) a.remote[t] = (uint16_t)((bstar & low) | ((bstar >> home) << (home + 1)));
 }
 
@@ -221,10 +239,14 @@ cobalt_status launch_assign(const DeviceLayout& L, const int32_t* topk, const in
     a.out = out;
     a.remote = remote;
     const unsigned blocks = (unsigned)((T + kAssignThreads - 1) / kAssignThreads);
+    const bool kv = K == 8 && ((uintptr_t)topk & 15u) == 0 && ((uintptr_t)out & 15u) == 0;
+    auto launch = [&](auto kernel) {
+        hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kAssignThreads), 0, s, a);
+    };
     if (L.N <= 9)
-        hipLaunchKernelGGL(assign_kernel<8>, dim3(blocks), dim3(kAssignThreads), 0, s, a);
+        kv ? launch(assign_kernel<8, true>) : launch(assign_kernel<8, false>);
     else
-        hipLaunchKernelGGL(assign_kernel<16>, dim3(blocks), dim3(kAssignThreads), 0, s, a);
+        kv ? launch(assign_kernel<16, true>) : launch(assign_kernel<16, false>);
     COBALT_LAUNCH_CHECK();
     return COBALT_OK;
 }
