@@ -21,7 +21,8 @@
  *    distinct experts per token, non-decreasing source ranks) are made only
  *    by cobalt_validate_routing: on data that fails them the path calls do
  *    not read or write outside the buffers they were given, but their
- *    results are unspecified.
+ *    results are unspecified (except where a call states them, as
+ *    cobalt_coact_stats does for repeated and out-of-range ids).
  *  - Calls on distinct (layout, stream, output buffers) may run concurrently.
  */
 #ifndef COBALT_H
