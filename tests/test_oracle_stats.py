@@ -61,3 +61,23 @@ def test_accumulates_across_calls():
 def test_rejects_out_of_range_ids():
     with pytest.raises(oracle.OracleError):
         oracle.coact_stats(np.array([[0, 9]], np.int32), 9)
+
+
+def test_repeated_ids_follow_the_ordered_slot_pair_definition():
+    """A token that holds an expert m times: every ordered pair of distinct
+    slots counts, so the diagonal entry gets m(m - 1) and a pair (i, j) the
+    product of the multiplicities. Counted here by hand on worked tokens."""
+    E = 6
+    topk = np.array([[2, 2, 2, 5],      # 2 three times: C[2][2] += 6; (2, 5) += 3 each way
+                     [1, 1, 4, 4],      # C[1][1] += 2, C[4][4] += 2; (1, 4) += 4 each way
+                     [0, 3, 3, 0]],     # C[0][0] += 2, C[3][3] += 2; (0, 3) += 4 each way
+                    np.int32)
+    C, cnt = oracle.coact_stats(topk, E)
+    want = np.zeros((E, E), np.uint32)
+    for i, j, v in [(2, 2, 6), (2, 5, 3), (5, 2, 3), (1, 1, 2), (4, 4, 2), (1, 4, 4), (4, 1, 4),
+                    (0, 0, 2), (3, 3, 2), (0, 3, 4), (3, 0, 4)]:
+        want[i, j] += v
+    assert np.array_equal(C, want)
+    assert cnt.tolist() == [2, 2, 3, 2, 2, 1]
+    # row sums stay (K - 1) * count with the diagonal included
+    assert np.array_equal(C.sum(1), 3 * cnt)
