@@ -415,3 +415,50 @@ def test_every_call_is_deterministic_over_ten_repeats():
             for a, b in zip(ref, got):
                 assert np.array_equal(a, b), f"repeat {rep} differs"
     st.close()
+
+
+def _random_topk(rng, T, E, K):
+    """T tokens of K distinct ids in [0, E), drawn without a T x E matrix."""
+    out = np.empty((T, K), np.int32)
+    need = np.arange(T)
+    draws = rng.integers(0, E, size=(T, K))
+    out[:] = draws
+    while True:
+        s = np.sort(out[need], axis=1)
+        dup = (s[:, 1:] == s[:, :-1]).any(1) if K > 1 else np.zeros(len(need), bool)
+        need = need[dup]
+        if not len(need):
+            return out
+        out[need] = rng.integers(0, E, size=(len(need), K))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_statistics_random_calls(seed):
+    """Random (T, E, K) up to T = 400 000 and E = 4096, with a few tokens
+    that repeat an id or hold an out-of-range one: the library against the
+    oracle on the tokens with ids in range plus the valid-slot brute force
+    on the others (the counts add over tokens)."""
+    rng = np.random.default_rng(1000 + seed)
+    for _ in range(4):
+        E = int(rng.choice([3, 16, 64, 255, 256, 384, 1000, 4096]))
+        K = int(rng.integers(1, min(16, E) + 1))
+        T = int(rng.choice([1, 1023, 4096, 65536, 131077, 262144, 400000]))
+        topk = _random_topk(rng, T, E, K)
+        bad = np.nonzero(rng.random(T) < 0.002)[0]
+        for r in bad:
+            if K > 1 and rng.random() < 0.5:
+                topk[r, int(rng.integers(1, K))] = topk[r, 0]
+            else:
+                topk[r, int(rng.integers(0, K))] = int(rng.choice([-1, E, E + 7]))
+        good = ((topk >= 0) & (topk < E)).all(1)
+        C, cnt = oracle.coact_stats(topk[good], E)
+        if (~good).any():
+            Cb, cb = _stats_valid_slots(topk[~good], E)
+            C = C + Cb
+            cnt = cnt + cb
+        print(f"statistics seed={seed} T={T} E={E} K={K} odd tokens={len(bad)}", flush=True)
+        coact = torch.zeros(E, E, dtype=torch.int32, device="cuda")
+        count = torch.zeros(E, dtype=torch.int32, device="cuda")
+        B.cobalt_coact_stats(dev_i32(topk), E, coact, count, B.stats_workspace_for(T, K, E))
+        assert np.array_equal(u32(coact), C)
+        assert np.array_equal(u32(count), cnt)

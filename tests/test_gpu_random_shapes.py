@@ -40,8 +40,8 @@ def _configs(n, seed=2024):
     return out
 
 
-# COBALT_RANDOM_SHAPES=n,seed draws another set (default: 24 shapes, seed 2024)
-_n, _seed = (int(v) for v in os.environ.get("COBALT_RANDOM_SHAPES", "24,2024").split(","))
+# COBALT_RANDOM_SHAPES=n,seed draws another set (default: 48 shapes, seed 2024)
+_n, _seed = (int(v) for v in os.environ.get("COBALT_RANDOM_SHAPES", "48,2024").split(","))
 CONFIGS = _configs(_n, _seed)
 
 
