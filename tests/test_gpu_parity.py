@@ -365,6 +365,21 @@ def test_replica_load_matches_oracle(name, T):
     assert np.array_equal(u32(load), ref)
 
 
+def test_replica_load_uint32_partials():
+    """Just over 64 chunks of 65535 pairs: the chunks' counts may pass
+    65535, so the partials are uint32 (T * K = 4 194 320, K = 8, E = 256,
+    G = 64), with a few pairs out of range."""
+    rng = np.random.default_rng(6)
+    T, K, E, G = 524290, 8, 256, 64
+    topk = rng.integers(0, E, size=(T, K)).astype(np.int32)
+    a = rng.integers(0, G, size=(T, K)).astype(np.int32)
+    a[rng.random((T, K)) < 1e-4] = G
+    load = torch.zeros(E, G, dtype=torch.int32, device="cuda")
+    B.cobalt_replica_load(dev_i32(topk), dev_i32(a), E, G, load,
+                          B.replica_load_workspace_for(T, K, E, G))
+    assert np.array_equal(u32(load), oracle.replica_load(topk, a, E, G))
+
+
 def test_replica_load_many_bands():
     """E * G beyond one LDS band (E = 4096, G = 32)."""
     rng = np.random.default_rng(4)
